@@ -1,0 +1,224 @@
+"""Encoder-stage forward + backward throughput on one MI355X.
+
+One step = stage_forward + stage_backward of a block of post-LN BERT encoder
+layers (every kernel of the hot path) over one batch of synthetic input
+already resident in HBM.  Default workload: 4 BERT-large-shaped layers
+(h 1024, 16 heads, FFN 4096), batch 32 x seq 512, no padding, bf16 storage
+with fp32 accumulation.
+
+Prints one JSON line: tokens/s, ms per step, TFLOP/s and fraction of the bf16
+MFMA peak, a roofline entry for the dominant kernel (timed with HIP events on
+the stage stream over the timed region), and the fp64 CPU oracle timed on a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6  # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def site_flops(site: str, cfg, lengths) -> float:
+    """Algorithmic FLOPs of one launch of a GEMM site (2 M N K)."""
+    T, h, f = cfg.batch * cfg.seq, cfg.hidden, cfg.ffn
+    S, H = cfg.seq, cfg.heads
+    table = {
+        "qkv_gemm_fwd": 2.0 * T * 3 * h * h,
+        "out_gemm_fwd": 2.0 * T * h * h,
+        "ffn1_gelu_gemm_fwd": 2.0 * T * f * h,
+        "ffn2_gemm_fwd": 2.0 * T * h * f,
+        "w2_wgrad_gemm": 2.0 * h * f * T,
+        "ffn2_dgrad_dgelu_gemm": 2.0 * T * f * h,
+        "w1_wgrad_gemm": 2.0 * f * h * T,
+        "ffn1_dgrad_resid_gemm": 2.0 * T * h * f,
+        "wo_wgrad_gemm": 2.0 * h * h * T,
+        "out_dgrad_gemm": 2.0 * T * h * h,
+        "wqkv_wgrad_gemm": 2.0 * 3 * h * h * T,
+        "qkv_dgrad_resid_gemm": 2.0 * T * h * 3 * h,
+    }
+    for k in ("scores_gemm_fwd", "context_gemm_fwd", "dp_gemm_bwd", "dv_gemm_bwd", "dq_gemm_bwd",
+              "dk_gemm_bwd"):
+        table[k] = 2.0 * cfg.batch * H * S * S * 64
+    return table.get(site, 0.0)
+
+
+def cpu_baseline(cfg, budget_s: float = 10.0):
+    """Time the fp64 oracle on whole sequences of the workload (same layers,
+    shapes and distributions), repeating until budget_s has elapsed."""
+    import numpy as np
+
+    import oracle
+    import synth
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    one = cfg.with_(batch=1)
+    params = synth.make_params(one)
+    inp = synth.make_inputs(one)
+    t0 = time.perf_counter()
+    n = 0
+    while True:
+        y, saved = oracle.stage_forward(inp["x"], inp["mask"], params, cfg.heads)
+        oracle.stage_backward(inp["dy"], saved, params)
+        n += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": n * cfg.seq / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{n} x one sequence of {cfg.seq} tokens through all {cfg.L} layers, "
+                      f"fwd+bwd, fp64 numpy ({dt:.1f} s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="bert_large_4")
+    ap.add_argument("--layers", type=int, default=None, help="override L (depth sweep)")
+    ap.add_argument("--roofline-site", default="ffn1_gelu_gemm_fwd")
+    ap.add_argument("--breakdown", action="store_true", help="per-site times to stderr")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=10.0)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(a stage shards by layers across GPUs; see the design notes).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2202_11836_amd import Stage, stage_site_count, stage_site_name
+
+    cfg = synth.CONFIGS[args.config]
+    if args.layers is not None:
+        cfg = cfg.with_(L=args.layers)
+    torch.cuda.set_device(0)
+    inp = synth.make_inputs(cfg)
+    dtype = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    x = torch.from_numpy(inp["x"].astype(np.float32)).to(dtype).cuda()
+    dy = torch.from_numpy(inp["dy"].astype(np.float32)).to(dtype).cuda()
+    mask = torch.from_numpy(inp["mask"]).cuda()
+    st = Stage(cfg.L, cfg.hidden, cfg.heads, cfg.ffn, seed=cfg.seed, dtype=cfg.dtype)
+    y = torch.empty_like(x)
+    dx = torch.empty_like(x)
+
+    def step():
+        st.forward(x, mask, out=y)
+        st.backward(dy, out=dx)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # Forward / backward split (paper reports them separately), untimed pass.
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    fwd_ms = bwd_ms = 0.0
+    for _ in range(3):
+        ev[0].record()
+        st.forward(x, mask, out=y)
+        ev[1].record()
+        st.backward(dy, out=dx)
+        ev[2].record()
+        torch.cuda.synchronize()
+        fwd_ms += ev[0].elapsed_time(ev[1]) / 3
+        bwd_ms += ev[1].elapsed_time(ev[2]) / 3
+
+    # Timed region; the dominant kernel's launches are traced with HIP events
+    # on the stage stream.
+    st.trace(args.roofline_site)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    launches, site_ms = st.trace_read()
+    st.trace(None)
+
+    ms_per_step = (t1 - t0) * 1000.0 / args.steps
+    tokens = cfg.batch * cfg.seq
+    flops = synth.flops_per_step(cfg, inp["lengths"] if cfg.len_lo is not None else None)
+    tflops = flops / (ms_per_step / 1000.0) / 1e12
+
+    per_launch_flops = site_flops(args.roofline_site, cfg, inp["lengths"])
+    avg_ms = site_ms / max(launches, 1)
+    achieved = per_launch_flops / (avg_ms / 1000.0) / 1e12 if launches else 0.0
+
+    if args.breakdown:
+        rows = []
+        for i in range(stage_site_count()):
+            name = stage_site_name(i)
+            st.trace(name)
+            step()
+            n, ms = st.trace_read()
+            rows.append((name, n, ms))
+        st.trace(None)
+        total = sum(r[2] for r in rows)
+        print(f"{'site':32s} {'launches':>8s} {'ms/step':>9s} {'share':>6s} {'TFLOP/s':>8s}",
+              file=sys.stderr)
+        for name, n, ms in sorted(rows, key=lambda r: -r[2]):
+            fl = site_flops(name, cfg, inp["lengths"]) * n
+            tf = fl / (ms / 1000.0) / 1e12 if ms > 0 and fl > 0 else 0.0
+            print(f"{name:32s} {n:8d} {ms:9.3f} {100 * ms / total:5.1f}% {tf:8.1f}", file=sys.stderr)
+        print(f"{'sum of kernels':32s} {'':8s} {total:9.3f}", file=sys.stderr)
+
+    out = {
+        "metric": "encoder-stage fwd+bwd tokens/s and % bf16 MFMA peak on 1 MI355X",
+        "value": tokens / (ms_per_step / 1000.0),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "fwd_ms": fwd_ms,
+        "bwd_ms": bwd_ms,
+        "tflops": tflops,
+        "pct_bf16_peak": 100.0 * tflops / PEAK_BF16_TFLOPS,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded N(0,1) inputs, N(0,0.02) weights; stands in for MNLI)",
+        "config": {
+            "workload": f"{cfg.name}: {cfg.L} post-LN encoder layers, h{cfg.hidden}, "
+                        f"{cfg.heads} heads, ffn {cfg.ffn}, B{cfg.batch} x S{cfg.seq}, "
+                        + ("no padding" if cfg.len_lo is None else
+                           f"valid lengths in [{cfg.len_lo},{cfg.len_hi}]"),
+            "L": cfg.L, "hidden": cfg.hidden, "heads": cfg.heads, "ffn": cfg.ffn,
+            "global_batch": cfg.batch, "seq_len": cfg.seq, "gflop_per_step": flops / 1e9,
+        },
+        "roofline": {
+            "kernel": args.roofline_site,
+            "bound": "mfma",
+            "achieved": achieved,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS,
+            "traffic": None,
+            "launches": launches,
+            "avg_launch_ms": avg_ms,
+            "flop_per_launch": per_launch_flops,
+        },
+    }
+    st.close()
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

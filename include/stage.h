@@ -1,0 +1,167 @@
+/*
+ * stage.h - C ABI of the MI355X (gfx950) encoder-stage library.
+ *
+ * A "stage" is a contiguous block of L post-LN BERT encoder layers that the
+ * layer allocator places on one device (paper section III: each device
+ * turns the previous device's output tensor into its own output, and after
+ * the forward pass computes its layers' gradients in reverse order).  One
+ * encoder layer (section II-C) is self-attention per Eq. (1),
+ * softmax(Q K^T / sqrt(d_k)) V with Q, K, V the input times three matrices,
+ * followed by three linear layers with residual connections: h -> h, h -> f
+ * (widening) and f -> h.  A LayerNorm follows each residual addition and the
+ * widening layer is followed by the exact erf GELU.
+ *
+ * Conventions
+ *   - Activations x, y, dy, dx are row-major [batch, seq, hidden] in the
+ *     stage dtype (fp32 or bf16), on the device, owned by the caller.
+ *   - key_mask is uint8 [batch, seq] on the device, owned by the caller;
+ *     1 = the key position may be attended, 0 = padding.  NULL = no padding.
+ *   - Parameters (per layer, in stage_param_id order) are owned by the
+ *     library: matrices in the stage dtype, row-major [out, in]; biases,
+ *     LayerNorm gammas and betas in fp32.  W_qkv stacks the query, key and
+ *     value matrices as row blocks [0,h), [h,2h), [2h,3h); head j owns
+ *     columns [64 j, 64 j + 64) of each projection.
+ *   - Gradients are fp32, owned by the library, overwritten (not
+ *     accumulated) by every stage_backward.
+ *   - All device work is enqueued on the stage's HIP stream; calls return
+ *     without synchronising unless stated.  Results are valid once the
+ *     caller has synchronised that stream.
+ *   - Every call returns a stage_status; nothing aborts or throws across
+ *     the ABI.  stage_last_error gives a message for the last failure.
+ */
+#ifndef SKY_STAGE_H
+#define SKY_STAGE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct stage stage_t; /* opaque, library-owned */
+
+typedef enum {
+  STAGE_OK = 0,
+  STAGE_EINVAL = 1, /* invalid argument: dims, null pointer, index range */
+  STAGE_ESTATE = 2, /* call out of order, e.g. backward without forward */
+  STAGE_ENOMEM = 3, /* device allocation failed */
+  STAGE_EHIP = 4    /* a HIP runtime call or kernel launch failed */
+} stage_status;
+
+typedef enum { STAGE_F32 = 0, STAGE_BF16 = 1 } stage_dtype;
+
+typedef enum {
+  STAGE_W_QKV = 0, /* [3h, h]  dtype */
+  STAGE_B_QKV = 1, /* [3h]     fp32  */
+  STAGE_W_O = 2,   /* [h, h]   dtype */
+  STAGE_B_O = 3,   /* [h]      fp32  */
+  STAGE_G1 = 4,    /* [h]      fp32, LayerNorm after attention */
+  STAGE_BE1 = 5,   /* [h]      fp32  */
+  STAGE_W_1 = 6,   /* [f, h]   dtype */
+  STAGE_B_1 = 7,   /* [f]      fp32  */
+  STAGE_W_2 = 8,   /* [h, f]   dtype */
+  STAGE_B_2 = 9,   /* [h]      fp32  */
+  STAGE_G2 = 10,   /* [h]      fp32, LayerNorm after the FFN */
+  STAGE_BE2 = 11,  /* [h]      fp32  */
+  STAGE_NPARAM = 12
+} stage_param_id;
+
+/* Saved activations of the latest forward pass (for layer-wise checks). */
+typedef enum {
+  STAGE_SAVED_X = 0,   /* layer input           [T, h]  dtype */
+  STAGE_SAVED_QKV = 1, /* Q | K | V             [T, 3h] dtype */
+  STAGE_SAVED_CTX = 2, /* attention context     [T, h]  dtype */
+  STAGE_SAVED_H1 = 3,  /* first LayerNorm out   [T, h]  dtype */
+  STAGE_SAVED_U = 4,   /* FFN pre-activation    [T, f]  dtype */
+  STAGE_SAVED_G = 5,   /* GELU(U)               [T, f]  dtype */
+  STAGE_NSAVED = 6
+} stage_saved_id;
+
+/*
+ * Create a stage of L_stage layers (sections II-C and III).
+ *   hidden: h, a multiple of 64, at most 2048;  heads: h / heads must be 64;
+ *   ffn: f, a multiple of 64.  seed: weights are drawn N(0, 0.02) by a
+ *   counter-based generator (splitmix64 of seed, layer, tensor and index,
+ *   Box-Muller) and rounded to dtype; biases and betas 0, gammas 1.
+ *   hip_stream: hipStream_t the stage enqueues on (NULL = default stream).
+ * On success *out owns device memory for parameters and gradients; release
+ * it with stage_destroy.  EINVAL on bad dims, ENOMEM / EHIP on failure (then
+ * *out is NULL).
+ */
+stage_status stage_init(int L_stage, int hidden, int heads, int ffn, uint64_t seed,
+                        stage_dtype dtype, void* hip_stream, stage_t** out);
+
+/* Change the stream later calls enqueue on. */
+stage_status stage_set_stream(stage_t* s, void* hip_stream);
+
+/*
+ * Forward pass of the stage (section III): y = layer_{L-1}(...layer_0(x)).
+ * x, y: [batch, seq, h] device, stage dtype; x and y may not alias.
+ * key_mask: [batch, seq] uint8 device or NULL.  batch, seq >= 0 (an empty
+ * batch is valid).  x and key_mask are copied into the saved context, so
+ * the caller may reuse them once the stream has passed this call.  The
+ * saved context replaces any earlier one.  (Activation buffers are
+ * (re)allocated when the token count grows.)
+ */
+stage_status stage_forward(stage_t* s, const void* x, const uint8_t* key_mask, int batch,
+                           int seq, void* y);
+
+/*
+ * Backward pass (section III: gradients in reverse layer order) of
+ * <y, dy> for the latest forward.  dy, dx: [batch, seq, h] device, stage
+ * dtype.  Writes dx and overwrites all parameter gradients.  Consumes the
+ * saved context: a second call without a new forward returns ESTATE.
+ */
+stage_status stage_backward(stage_t* s, const void* dy, void* dx);
+
+/* Device pointer, element count and dtype of parameter `which` of `layer`. */
+stage_status stage_param(stage_t* s, int layer, int which, void** dev_ptr, int64_t* numel,
+                         stage_dtype* dtype);
+
+/* Device pointer (fp32) and element count of that parameter's gradient. */
+stage_status stage_grad(stage_t* s, int layer, int which, float** dev_ptr, int64_t* numel);
+
+/*
+ * Copy `bytes` bytes from src (host or device) into parameter `which` of
+ * `layer` (bytes must equal numel * element size of its dtype).
+ * Synchronises the stage stream before returning.
+ */
+stage_status stage_set_param(stage_t* s, int layer, int which, const void* src, size_t bytes);
+
+/*
+ * Copy a library-owned tensor into dst (host or device), synchronously on
+ * the stage stream.  kind 0 = parameter, 1 = gradient, 2 = saved activation
+ * (stage_saved_id; needs a saved context).  bytes must equal the tensor's
+ * size in bytes (fp32 for gradients).
+ */
+stage_status stage_read(stage_t* s, int kind, int layer, int which, void* dst, size_t bytes);
+
+/* Bytes of the tensor stage_read(kind, layer, which) would copy (0 if none). */
+size_t stage_tensor_bytes(stage_t* s, int kind, int layer, int which);
+
+/*
+ * Tracing (the paper times forward and backward work per module to profile
+ * devices, section V-B).  stage_trace_site(s, site) makes every later launch
+ * of kernel site `site` (0 <= site < stage_site_count(); -1 = off) record a
+ * pair of HIP events on the stage stream around it, and clears earlier
+ * records.  stage_trace_read synchronises the stream and returns how many
+ * traced launches ran and their summed event time in ms, then clears the
+ * records.  Tracing adds two event records per traced launch and nothing
+ * to untraced ones.
+ */
+stage_status stage_trace_site(stage_t* s, int site);
+stage_status stage_trace_read(stage_t* s, int* launches, double* total_ms);
+int stage_site_count(void);
+const char* stage_site_name(int site); /* "" for an unknown site */
+
+/* Message describing the last failure on this handle ("" if none). */
+const char* stage_last_error(const stage_t* s);
+
+/* Free everything the handle owns (synchronises its stream). NULL is a no-op. */
+void stage_destroy(stage_t* s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SKY_STAGE_H */

@@ -1,0 +1,94 @@
+// Host-side launchers of the encoder-stage kernels (gfx950).  Every launcher
+// enqueues on the given stream and returns the launch status; none of them
+// synchronises.  Shapes are validated by the caller (the stage engine).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+
+// ---------------------------------------------------------------------------
+// GEMM:  C[m, n] = sum_k A(m, k) * B(k, n), then an epilogue.
+//   A(m, k) = A[m * lda + k]  if a_kmajor  else  A[k * lda + m]
+//   B(k, n) = B[n * ldb + k]  if b_kmajor  else  B[k * ldb + n]
+// Batched over grid z: batch index zb splits into (zb / zdiv, zb % zdiv),
+// and each operand is offset by (zb / zdiv) * s*1 + (zb % zdiv) * s*2.
+// With ksplit > 1 the K range is cut into ksplit chunks of kchunk elements
+// and each chunk writes an fp32 partial to C + split * M * ldc (EPI_PARTIAL).
+// ---------------------------------------------------------------------------
+enum GemmEpi {
+  EPI_STORE = 0,    // C = alpha * acc (+ bias[n] when bias != nullptr)
+  EPI_GELU = 1,     // U = acc + bias[n] -> C;  GELU(U) -> C2
+  EPI_DGELU = 2,    // C = acc * GELU'(aux[m, n])
+  EPI_RESID = 3,    // C = acc + aux[m, n]
+  EPI_PARTIAL = 4,  // fp32 C[split][m][n] = acc over this split's K range
+};
+
+struct GemmArgs {
+  const void* A;
+  const void* B;
+  void* C;
+  void* C2;
+  const float* bias;
+  const void* aux;
+  int M, N, K;
+  int64_t lda, ldb, ldc, ldaux;
+  int zdiv;
+  int64_t sA1, sA2, sB1, sB2, sC1, sC2;
+  int ksplit;
+  int kchunk;
+  float alpha;
+};
+
+inline GemmArgs gemm_args(const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
+                          int64_t ldc, int M, int N, int K) {
+  GemmArgs g{};
+  g.A = A; g.B = B; g.C = C; g.lda = lda; g.ldb = ldb; g.ldc = ldc;
+  g.M = M; g.N = N; g.K = K; g.zdiv = 1; g.ksplit = 1; g.kchunk = K; g.alpha = 1.0f;
+  return g;
+}
+
+// bf16 operands on MFMA (fp32 accumulation).  out_f32 selects fp32 output
+// for EPI_STORE; all other epilogues write bf16 (EPI_PARTIAL writes fp32).
+hipError_t gemm_bf16(const GemmArgs& g, bool a_kmajor, bool b_kmajor, GemmEpi epi,
+                     bool out_f32, int batch, hipStream_t st);
+// fp32 operands on the vector ALU (fp32 accumulation), same conventions.
+hipError_t gemm_f32(const GemmArgs& g, bool a_kmajor, bool b_kmajor, GemmEpi epi,
+                    int batch, hipStream_t st);
+// out[m][n] = sum_s part[s][m][n] (fixed order), fp32.
+hipError_t splitk_reduce(const float* part, int splits, int M, int N, float* out, hipStream_t st);
+
+// ---------------------------------------------------------------------------
+// Row kernels (one wavefront per row), T = float or bf16_t.
+// ---------------------------------------------------------------------------
+// z = a + bias + resid;  y = gamma * xhat + beta with xhat = (z - mean) * rstd.
+template <typename T>
+hipError_t add_ln_fwd(const T* a, const float* bias, const T* resid, const float* gamma,
+                      const float* beta, T* y, T* xhat, float* rstd, int rows, int h,
+                      hipStream_t st);
+
+// dz = rstd * (g - mean(g) - xhat * mean(g * xhat)), g = dy * gamma.
+// Column partial sums per row block: part[blk][0][:] = sum dy*xhat,
+// part[blk][1][:] = sum dy, part[blk][2][:] = sum dz.
+template <typename T>
+hipError_t ln_bwd(const T* dy, const T* xhat, const float* rstd, const float* gamma, T* dz,
+                  float* part, int nblk, int rows, int h, hipStream_t st);
+
+// part[blk][n] = sum over the block's rows of x[row][n].
+template <typename T>
+hipError_t col_partial(const T* x, int rows, int n, float* part, int nblk, hipStream_t st);
+
+// out[c][n] = sum_blk part[blk][c][n] for c < nvec (fixed order).
+hipError_t col_reduce(const float* part, int nblk, int nvec, int n, float* const* outs,
+                      hipStream_t st);
+
+// ---------------------------------------------------------------------------
+// Attention row kernels on a materialised score matrix.
+// scores/dP: fp32 [B*H][S][ld]; P, dS: T [B*H][S][ld]; mask: uint8 [B][S].
+// ---------------------------------------------------------------------------
+template <typename T>
+hipError_t softmax_fwd(const float* scores, const uint8_t* mask, T* P, int BH, int H, int S,
+                       int ld, float scale, hipStream_t st);
+template <typename T>
+hipError_t softmax_bwd(const float* dP, const T* P, T* dS, int BH, int S, int ld, float scale,
+                       hipStream_t st);

@@ -1,0 +1,793 @@
+// Stage engine and C ABI: owns parameters, gradients, the saved-activation
+// record of the latest forward pass and the workspace, and sequences the
+// per-layer kernel launches of one pipeline stage on one HIP stream
+// (paper section III: forward through the device's layers, then gradients
+// in reverse layer order).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <array>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/stage.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr int HEAD_DIM = 64;
+constexpr int LN_PARTS = 256;  // wavefront partials of the LayerNorm backward
+constexpr int COL_PARTS = 128; // row blocks of the bias-gradient column sums
+
+// Kernel launch sites of one layer, for event tracing (stage_trace_site).
+#define STAGE_SITES(X)                                                              \
+  X(QKV_FWD, "qkv_gemm_fwd") X(SCORES_FWD, "scores_gemm_fwd")                         \
+  X(SOFTMAX_FWD, "softmax_fwd") X(CTX_FWD, "context_gemm_fwd")                        \
+  X(OUT_FWD, "out_gemm_fwd") X(LN1_FWD, "add_ln1_fwd") X(FFN1_FWD, "ffn1_gelu_gemm_fwd") \
+  X(FFN2_FWD, "ffn2_gemm_fwd") X(LN2_FWD, "add_ln2_fwd") X(LN2_BWD, "ln2_bwd")          \
+  X(LN2_RED, "ln2_bwd_colreduce") X(W2_WGRAD, "w2_wgrad_gemm")                          \
+  X(W2_RED, "w2_wgrad_splitk_reduce") X(FFN2_DGRAD, "ffn2_dgrad_dgelu_gemm")            \
+  X(B1_SUM, "b1_colsum") X(B1_RED, "b1_colreduce") X(W1_WGRAD, "w1_wgrad_gemm")         \
+  X(W1_RED, "w1_wgrad_splitk_reduce") X(FFN1_DGRAD, "ffn1_dgrad_resid_gemm")            \
+  X(LN1_BWD, "ln1_bwd") X(LN1_RED, "ln1_bwd_colreduce") X(WO_WGRAD, "wo_wgrad_gemm")    \
+  X(WO_RED, "wo_wgrad_splitk_reduce") X(OUT_DGRAD, "out_dgrad_gemm")                    \
+  X(DP_BWD, "dp_gemm_bwd") X(SOFTMAX_BWD, "softmax_bwd") X(DV_BWD, "dv_gemm_bwd")        \
+  X(DQ_BWD, "dq_gemm_bwd") X(DK_BWD, "dk_gemm_bwd") X(BQKV_SUM, "bqkv_colsum")           \
+  X(BQKV_RED, "bqkv_colreduce") X(WQKV_WGRAD, "wqkv_wgrad_gemm")                        \
+  X(WQKV_RED, "wqkv_wgrad_splitk_reduce") X(QKV_DGRAD, "qkv_dgrad_resid_gemm")
+
+enum Site {
+#define SITE_ENUM(id, name) SITE_##id,
+  STAGE_SITES(SITE_ENUM)
+#undef SITE_ENUM
+  SITE_COUNT
+};
+const char* const SITE_NAMES[] = {
+#define SITE_NAME(id, name) name,
+    STAGE_SITES(SITE_NAME)
+#undef SITE_NAME
+};
+
+// --------------------------------------------------------------------------
+// Parameter initialisation: counter-based splitmix64 (Steele, Lea & Flood,
+// "Fast splittable pseudorandom number generators", 2014) feeding two 53-bit
+// uniforms into Box-Muller.
+// --------------------------------------------------------------------------
+__host__ __device__ inline uint64_t splitmix64_mix(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+constexpr uint64_t GOLDEN = 0x9E3779B97F4A7C15ull;
+
+template <typename T>
+__global__ void init_normal_kernel(T* out, int64_t n, uint64_t key, double stdv) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  uint64_t a = splitmix64_mix(key + (uint64_t)(2 * i + 1) * GOLDEN);
+  uint64_t b = splitmix64_mix(key + (uint64_t)(2 * i + 2) * GOLDEN);
+  double u1 = ((double)(a >> 11) + 1.0) * (1.0 / 9007199254740992.0);  // (0, 1]
+  double u2 = (double)(b >> 11) * (1.0 / 9007199254740992.0);          // [0, 1)
+  double z = sqrt(-2.0 * log(u1)) * cos(6.283185307179586 * u2);
+  st_f(out + i, (float)(z * stdv));
+}
+
+__global__ void fill_kernel(float* out, int64_t n, float v) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) out[i] = v;
+}
+
+__global__ void ones_u8_kernel(uint8_t* out, int64_t n) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) out[i] = 1;
+}
+
+bool is_matrix(int which) {
+  return which == STAGE_W_QKV || which == STAGE_W_O || which == STAGE_W_1 || which == STAGE_W_2;
+}
+
+struct Saved {
+  void* X = nullptr;     // layer input [T, h]
+  void* QKV = nullptr;   // [T, 3h]
+  void* P = nullptr;     // softmax probabilities [B*H, S, S]
+  void* C = nullptr;     // context [T, h]
+  void* xhat1 = nullptr; // [T, h]
+  float* rstd1 = nullptr;
+  void* H1 = nullptr;    // [T, h]
+  void* U = nullptr;     // [T, f]
+  void* G = nullptr;     // [T, f]
+  void* xhat2 = nullptr; // [T, h]
+  float* rstd2 = nullptr;
+};
+
+}  // namespace
+
+struct stage {
+  int L = 0, h = 0, H = 0, f = 0;
+  stage_dtype dtype = STAGE_F32;
+  size_t esz = 4;
+  hipStream_t stream = nullptr;
+  std::vector<std::array<void*, STAGE_NPARAM>> param;
+  std::vector<std::array<float*, STAGE_NPARAM>> grad;
+  std::vector<void*> allocs;  // parameter / gradient memory
+
+  // Activation memory, sized for cap_T tokens and cap_BSS score entries.
+  int64_t cap_T = -1, cap_BSS = -1;
+  std::vector<void*> act_allocs;
+  std::vector<Saved> saved;
+  uint8_t* mask = nullptr;
+  void* tmp = nullptr;      // [T, h] GEMM output before LayerNorm
+  float* scores = nullptr;  // [B*H, S, S] fp32 (scores, then dP)
+  void* dS = nullptr;       // [B*H, S, S]
+  void* dQKV = nullptr;     // [T, 3h]
+  void* dZ2 = nullptr;      // [T, h]
+  void* dU = nullptr;       // [T, f]
+  void* dH1 = nullptr;      // [T, h]
+  void* dZ1 = nullptr;      // [T, h]
+  void* dC = nullptr;       // [T, h]
+  void* dY = nullptr;       // [T, h] gradient flowing between layers
+  float* part = nullptr;    // column-sum partials
+  float* splitk = nullptr;  // split-K partials of the weight gradients
+  size_t splitk_elems = 0;
+
+  int B = 0, S = 0;
+  bool have_ctx = false;
+  std::string err;
+
+  // Event tracing of one launch site.
+  int trace_site = -1;
+  std::vector<hipEvent_t> events;  // pool, reused
+  size_t events_used = 0;
+};
+
+namespace {
+
+stage_status fail(stage_t* s, stage_status st, const std::string& msg) {
+  if (s) s->err = msg;
+  return st;
+}
+
+#define HIPCK(expr)                                                                    \
+  do {                                                                                 \
+    hipError_t e_ = (expr);                                                            \
+    if (e_ != hipSuccess)                                                              \
+      return fail(s, STAGE_EHIP, std::string(#expr) + ": " + hipGetErrorString(e_));   \
+  } while (0)
+
+// Records a start event before a traced site's launch; returns the pool
+// index of the event pair, or -1 when the site is not traced.
+int trace_begin(stage_t* s, int site) {
+  if (s->trace_site != site) return -1;
+  while (s->events.size() < s->events_used + 2) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return -1;
+    s->events.push_back(e);
+  }
+  int idx = (int)s->events_used;
+  s->events_used += 2;
+  if (hipEventRecord(s->events[idx], s->stream) != hipSuccess) {
+    s->events_used -= 2;
+    return -1;
+  }
+  return idx;
+}
+void trace_end(stage_t* s, int idx) {
+  if (idx < 0) return;
+  (void)hipEventRecord(s->events[idx + 1], s->stream);
+}
+
+// Launch expression `expr` (a hipError_t) as traced site number `site`.
+#define SITE_I(site, expr)                                                        \
+  do {                                                                            \
+    int tr_ = trace_begin(s, (site));                                             \
+    hipError_t e_ = (expr);                                                       \
+    trace_end(s, tr_);                                                            \
+    if (e_ != hipSuccess)                                                         \
+      return fail(s, STAGE_EHIP,                                                  \
+                  std::string(SITE_NAMES[(site)]) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+#define SITE(id, expr) SITE_I(SITE_##id, expr)
+
+int64_t param_numel(const stage_t* s, int which) {
+  const int64_t h = s->h, f = s->f;
+  switch (which) {
+    case STAGE_W_QKV: return 3 * h * h;
+    case STAGE_B_QKV: return 3 * h;
+    case STAGE_W_O: return h * h;
+    case STAGE_W_1: return f * h;
+    case STAGE_B_1: return f;
+    case STAGE_W_2: return h * f;
+    default: return h;
+  }
+}
+
+size_t param_esz(const stage_t* s, int which) { return is_matrix(which) ? s->esz : 4; }
+
+void free_activations(stage_t* s) {
+  for (void* p : s->act_allocs) (void)hipFree(p);
+  s->act_allocs.clear();
+  s->saved.clear();
+  s->cap_T = s->cap_BSS = -1;
+  s->have_ctx = false;
+}
+
+stage_status dev_alloc(stage_t* s, std::vector<void*>& list, void** p, size_t bytes) {
+  *p = nullptr;
+  if (bytes == 0) bytes = 256;
+  hipError_t e = hipMalloc(p, bytes);
+  if (e != hipSuccess) {
+    *p = nullptr;
+    (void)hipGetLastError();
+    return fail(s, STAGE_ENOMEM, std::string("hipMalloc(") + std::to_string(bytes) +
+                                     " bytes): " + hipGetErrorString(e));
+  }
+  list.push_back(*p);
+  return STAGE_OK;
+}
+
+// Number of K splits for a weight-gradient GEMM with reduction length K over
+// `tiles` output tiles: enough work-groups to cover the chip, chunks of at
+// least 256 rows.
+int choose_ksplit(int64_t tiles, int K) {
+  int ks = 1;
+  while (tiles * ks < 512 && K / (ks * 2) >= 256 && ks < 32) ks *= 2;
+  return ks;
+}
+
+stage_status ensure_activations(stage_t* s, int B, int S) {
+  const int64_t T = (int64_t)B * S;
+  const int64_t BSS = (int64_t)B * s->H * S * S;
+  if (T <= s->cap_T && BSS <= s->cap_BSS && (int)s->saved.size() == s->L) return STAGE_OK;
+  free_activations(s);
+  const size_t e = s->esz;
+  const int64_t h = s->h, f = s->f;
+  auto A = [&](void** p, size_t bytes) { return dev_alloc(s, s->act_allocs, p, bytes); };
+  stage_status st;
+  s->saved.resize(s->L);
+  for (int l = 0; l < s->L; ++l) {
+    Saved& v = s->saved[l];
+    if ((st = A(&v.X, T * h * e)) || (st = A(&v.QKV, T * 3 * h * e)) ||
+        (st = A(&v.P, BSS * e)) || (st = A(&v.C, T * h * e)) || (st = A(&v.xhat1, T * h * e)) ||
+        (st = A((void**)&v.rstd1, T * 4)) || (st = A(&v.H1, T * h * e)) ||
+        (st = A(&v.U, T * f * e)) || (st = A(&v.G, T * f * e)) ||
+        (st = A(&v.xhat2, T * h * e)) || (st = A((void**)&v.rstd2, T * 4)))
+      return st;
+  }
+  if ((st = A((void**)&s->mask, T)) || (st = A(&s->tmp, T * h * e)) ||
+      (st = A((void**)&s->scores, BSS * 4)) || (st = A(&s->dS, BSS * e)) ||
+      (st = A(&s->dQKV, T * 3 * h * e)) || (st = A(&s->dZ2, T * h * e)) ||
+      (st = A(&s->dU, T * f * e)) || (st = A(&s->dH1, T * h * e)) ||
+      (st = A(&s->dZ1, T * h * e)) || (st = A(&s->dC, T * h * e)) || (st = A(&s->dY, T * h * e)))
+    return st;
+  const int64_t maxw = std::max<int64_t>(3 * h, f);
+  const int64_t part_elems = std::max<int64_t>((int64_t)LN_PARTS * 3 * h, (int64_t)COL_PARTS * maxw);
+  if ((st = A((void**)&s->part, part_elems * 4))) return st;
+  // Split-K partials: largest weight gradient times its split count.
+  size_t need = 0;
+  const int64_t shapes[4][2] = {{3 * h, h}, {h, h}, {f, h}, {h, f}};
+  for (auto& mn : shapes) {
+    int64_t tiles = ((mn[0] + 127) / 128) * ((mn[1] + 127) / 128);
+    int ks = choose_ksplit(tiles, (int)T);
+    if (ks > 1) need = std::max<size_t>(need, (size_t)ks * mn[0] * mn[1]);
+  }
+  s->splitk_elems = need;
+  if ((st = A((void**)&s->splitk, std::max<size_t>(need, 1) * 4))) return st;
+  s->cap_T = T;
+  s->cap_BSS = BSS;
+  return STAGE_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Typed launch helpers
+// ---------------------------------------------------------------------------
+template <typename T> struct Gemm;
+template <> struct Gemm<bf16_t> {
+  static hipError_t run(const GemmArgs& g, bool ak, bool bk, GemmEpi epi, bool out_f32, int batch,
+                        hipStream_t st) {
+    return gemm_bf16(g, ak, bk, epi, out_f32, batch, st);
+  }
+};
+template <> struct Gemm<float> {
+  static hipError_t run(const GemmArgs& g, bool ak, bool bk, GemmEpi epi, bool, int batch,
+                        hipStream_t st) {
+    return gemm_f32(g, ak, bk, epi, batch, st);
+  }
+};
+
+// Weight gradient dW[M, N] = sum_t dY[t, m] * X[t, n] (fp32 out), split over
+// t when the output has few tiles; the split partials are summed in order.
+template <typename T>
+stage_status wgrad(stage_t* s, int site, int site_red, const T* dYm, int64_t ld_dy, const T* Xn,
+                   int64_t ld_x, int M, int N, int Tk, float* out) {
+  GemmArgs g = gemm_args(dYm, ld_dy, Xn, ld_x, out, N, M, N, Tk);
+  int64_t tiles = (int64_t)((M + 127) / 128) * ((N + 127) / 128);
+  int ks = choose_ksplit(tiles, Tk);
+  if (ks > 1 && (size_t)ks * M * N <= s->splitk_elems) {
+    int chunk = (Tk + ks - 1) / ks;
+    chunk = (chunk + 63) / 64 * 64;
+    ks = (Tk + chunk - 1) / chunk;
+    g.C = s->splitk;
+    g.ksplit = ks;
+    g.kchunk = chunk;
+    SITE_I(site, Gemm<T>::run(g, false, false, EPI_PARTIAL, true, 1, s->stream));
+    SITE_I(site_red, splitk_reduce(s->splitk, ks, M, N, out, s->stream));
+  } else {
+    SITE_I(site, Gemm<T>::run(g, false, false, EPI_STORE, true, 1, s->stream));
+  }
+  return STAGE_OK;
+}
+
+template <typename T>
+stage_status forward_impl(stage_t* s, const T* x, T* y) {
+  const int B = s->B, S = s->S, h = s->h, H = s->H, f = s->f;
+  const int Tn = B * S;
+  const int BH = B * H;
+  hipStream_t st = s->stream;
+  const float scale = 1.0f / sqrtf((float)HEAD_DIM);
+  HIPCK(hipMemcpyAsync(s->saved[0].X, x, (size_t)Tn * h * sizeof(T), hipMemcpyDeviceToDevice, st));
+  for (int l = 0; l < s->L; ++l) {
+    Saved& v = s->saved[l];
+    auto& p = s->param[l];
+    const T* X = (const T*)v.X;
+    T* QKV = (T*)v.QKV;
+    // QKV = X W_qkv^T + b_qkv
+    {
+      GemmArgs g = gemm_args(X, h, p[STAGE_W_QKV], h, QKV, 3 * h, Tn, 3 * h, h);
+      g.bias = (const float*)p[STAGE_B_QKV];
+      SITE(QKV_FWD, Gemm<T>::run(g, true, true, EPI_STORE, false, 1, st));
+    }
+    // scores[b, j] = Q_bj K_bj^T  (fp32)
+    {
+      GemmArgs g = gemm_args(QKV, 3 * h, QKV + h, 3 * h, s->scores, S, S, S, HEAD_DIM);
+      g.zdiv = H;
+      g.sA1 = g.sB1 = (int64_t)S * 3 * h;
+      g.sA2 = g.sB2 = HEAD_DIM;
+      g.sC1 = (int64_t)H * S * S;
+      g.sC2 = (int64_t)S * S;
+      SITE(SCORES_FWD, Gemm<T>::run(g, true, true, EPI_STORE, true, BH, st));
+    }
+    SITE(SOFTMAX_FWD, softmax_fwd<T>(s->scores, s->mask, (T*)v.P, BH, H, S, S, scale, st));
+    // C[b, :, j] = P_bj V_bj
+    {
+      GemmArgs g = gemm_args(v.P, S, QKV + 2 * h, 3 * h, v.C, h, S, HEAD_DIM, S);
+      g.zdiv = H;
+      g.sA1 = (int64_t)H * S * S;
+      g.sA2 = (int64_t)S * S;
+      g.sB1 = (int64_t)S * 3 * h;
+      g.sB2 = HEAD_DIM;
+      g.sC1 = (int64_t)S * h;
+      g.sC2 = HEAD_DIM;
+      SITE(CTX_FWD, Gemm<T>::run(g, true, false, EPI_STORE, false, BH, st));
+    }
+    // tmp = C W_o^T;  H1 = LN(X + tmp + b_o)
+    {
+      GemmArgs g = gemm_args(v.C, h, p[STAGE_W_O], h, s->tmp, h, Tn, h, h);
+      SITE(OUT_FWD, Gemm<T>::run(g, true, true, EPI_STORE, false, 1, st));
+    }
+    SITE(LN1_FWD, add_ln_fwd<T>((const T*)s->tmp, (const float*)p[STAGE_B_O], X,
+                        (const float*)p[STAGE_G1], (const float*)p[STAGE_BE1], (T*)v.H1,
+                        (T*)v.xhat1, v.rstd1, Tn, h, st));
+    // U = H1 W_1^T + b_1;  G = GELU(U)
+    {
+      GemmArgs g = gemm_args(v.H1, h, p[STAGE_W_1], h, v.U, f, Tn, f, h);
+      g.bias = (const float*)p[STAGE_B_1];
+      g.C2 = v.G;
+      SITE(FFN1_FWD, Gemm<T>::run(g, true, true, EPI_GELU, false, 1, st));
+    }
+    // tmp = G W_2^T;  Y = LN(H1 + tmp + b_2)
+    {
+      GemmArgs g = gemm_args(v.G, f, p[STAGE_W_2], f, s->tmp, h, Tn, h, f);
+      SITE(FFN2_FWD, Gemm<T>::run(g, true, true, EPI_STORE, false, 1, st));
+    }
+    T* Y = (l + 1 < s->L) ? (T*)s->saved[l + 1].X : y;
+    SITE(LN2_FWD, add_ln_fwd<T>((const T*)s->tmp, (const float*)p[STAGE_B_2], (const T*)v.H1,
+                        (const float*)p[STAGE_G2], (const float*)p[STAGE_BE2], Y, (T*)v.xhat2,
+                        v.rstd2, Tn, h, st));
+  }
+  return STAGE_OK;
+}
+
+template <typename T>
+stage_status ln_backward(stage_t* s, int site, int site_red, const T* dy, const T* xhat, const float* rstd,
+                         const float* gamma, T* dz, float* dgamma, float* dbeta, float* dbias) {
+  const int Tn = s->B * s->S, h = s->h;
+  SITE_I(site, ln_bwd<T>(dy, xhat, rstd, gamma, dz, s->part, LN_PARTS, Tn, h, s->stream));
+  float* outs[3] = {dgamma, dbeta, dbias};
+  SITE_I(site_red, col_reduce(s->part, LN_PARTS, 3, h, outs, s->stream));
+  return STAGE_OK;
+}
+
+template <typename T>
+stage_status col_sum(stage_t* s, int site, int site_red, const T* x, int n, float* out) {
+  const int Tn = s->B * s->S;
+  SITE_I(site, col_partial<T>(x, Tn, n, s->part, COL_PARTS, s->stream));
+  float* outs[1] = {out};
+  SITE_I(site_red, col_reduce(s->part, COL_PARTS, 1, n, outs, s->stream));
+  return STAGE_OK;
+}
+
+template <typename T>
+stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
+  const int B = s->B, S = s->S, h = s->h, H = s->H, f = s->f;
+  const int Tn = B * S;
+  const int BH = B * H;
+  hipStream_t st = s->stream;
+  const float scale = 1.0f / sqrtf((float)HEAD_DIM);
+  stage_status r;
+  const T* dYcur = dy;
+  for (int l = s->L - 1; l >= 0; --l) {
+    Saved& v = s->saved[l];
+    auto& p = s->param[l];
+    auto& gr = s->grad[l];
+    T* dZ2 = (T*)s->dZ2;
+    T* dU = (T*)s->dU;
+    T* dH1 = (T*)s->dH1;
+    T* dZ1 = (T*)s->dZ1;
+    T* dC = (T*)s->dC;
+    T* dQKV = (T*)s->dQKV;
+    const T* QKV = (const T*)v.QKV;
+    // Y = LN(Z2): dZ2, dgamma2, dbeta2, and db_2 = sum_t dZ2
+    if ((r = ln_backward<T>(s, SITE_LN2_BWD, SITE_LN2_RED, dYcur, (const T*)v.xhat2, v.rstd2, (const float*)p[STAGE_G2], dZ2,
+                            gr[STAGE_G2], gr[STAGE_BE2], gr[STAGE_B_2])))
+      return r;
+    // dW_2 = dZ2^T G
+    if ((r = wgrad<T>(s, SITE_W2_WGRAD, SITE_W2_RED, dZ2, h, (const T*)v.G, f, h, f, Tn, gr[STAGE_W_2]))) return r;
+    // dU = (dZ2 W_2) * GELU'(U)
+    {
+      GemmArgs g = gemm_args(dZ2, h, p[STAGE_W_2], f, dU, f, Tn, f, h);
+      g.aux = v.U;
+      g.ldaux = f;
+      SITE(FFN2_DGRAD, Gemm<T>::run(g, true, false, EPI_DGELU, false, 1, st));
+    }
+    if ((r = col_sum<T>(s, SITE_B1_SUM, SITE_B1_RED, dU, f, gr[STAGE_B_1]))) return r;
+    // dW_1 = dU^T H1
+    if ((r = wgrad<T>(s, SITE_W1_WGRAD, SITE_W1_RED, dU, f, (const T*)v.H1, h, f, h, Tn, gr[STAGE_W_1]))) return r;
+    // dH1 = dZ2 + dU W_1
+    {
+      GemmArgs g = gemm_args(dU, f, p[STAGE_W_1], h, dH1, h, Tn, h, f);
+      g.aux = dZ2;
+      g.ldaux = h;
+      SITE(FFN1_DGRAD, Gemm<T>::run(g, true, false, EPI_RESID, false, 1, st));
+    }
+    // H1 = LN(Z1): dZ1, dgamma1, dbeta1, db_o
+    if ((r = ln_backward<T>(s, SITE_LN1_BWD, SITE_LN1_RED, dH1, (const T*)v.xhat1, v.rstd1, (const float*)p[STAGE_G1], dZ1,
+                            gr[STAGE_G1], gr[STAGE_BE1], gr[STAGE_B_O])))
+      return r;
+    // dW_o = dZ1^T C
+    if ((r = wgrad<T>(s, SITE_WO_WGRAD, SITE_WO_RED, dZ1, h, (const T*)v.C, h, h, h, Tn, gr[STAGE_W_O]))) return r;
+    // dC = dZ1 W_o
+    {
+      GemmArgs g = gemm_args(dZ1, h, p[STAGE_W_O], h, dC, h, Tn, h, h);
+      SITE(OUT_DGRAD, Gemm<T>::run(g, true, false, EPI_STORE, false, 1, st));
+    }
+    // dP[b, j] = dC_bj V_bj^T (fp32, into the score buffer)
+    {
+      GemmArgs g = gemm_args(dC, h, QKV + 2 * h, 3 * h, s->scores, S, S, S, HEAD_DIM);
+      g.zdiv = H;
+      g.sA1 = (int64_t)S * h;
+      g.sA2 = HEAD_DIM;
+      g.sB1 = (int64_t)S * 3 * h;
+      g.sB2 = HEAD_DIM;
+      g.sC1 = (int64_t)H * S * S;
+      g.sC2 = (int64_t)S * S;
+      SITE(DP_BWD, Gemm<T>::run(g, true, true, EPI_STORE, true, BH, st));
+    }
+    // dS = scale * P * (dP - rowsum(dP * P))
+    SITE(SOFTMAX_BWD, softmax_bwd<T>(s->scores, (const T*)v.P, (T*)s->dS, BH, S, S, scale, st));
+    // dV_bj = P_bj^T dC_bj
+    {
+      GemmArgs g = gemm_args(v.P, S, dC, h, dQKV + 2 * h, 3 * h, S, HEAD_DIM, S);
+      g.zdiv = H;
+      g.sA1 = (int64_t)H * S * S;
+      g.sA2 = (int64_t)S * S;
+      g.sB1 = (int64_t)S * h;
+      g.sB2 = HEAD_DIM;
+      g.sC1 = (int64_t)S * 3 * h;
+      g.sC2 = HEAD_DIM;
+      SITE(DV_BWD, Gemm<T>::run(g, false, false, EPI_STORE, false, BH, st));
+    }
+    // dQ_bj = dS_bj K_bj
+    {
+      GemmArgs g = gemm_args(s->dS, S, QKV + h, 3 * h, dQKV, 3 * h, S, HEAD_DIM, S);
+      g.zdiv = H;
+      g.sA1 = (int64_t)H * S * S;
+      g.sA2 = (int64_t)S * S;
+      g.sB1 = (int64_t)S * 3 * h;
+      g.sB2 = HEAD_DIM;
+      g.sC1 = (int64_t)S * 3 * h;
+      g.sC2 = HEAD_DIM;
+      SITE(DQ_BWD, Gemm<T>::run(g, true, false, EPI_STORE, false, BH, st));
+    }
+    // dK_bj = dS_bj^T Q_bj
+    {
+      GemmArgs g = gemm_args(s->dS, S, QKV, 3 * h, dQKV + h, 3 * h, S, HEAD_DIM, S);
+      g.zdiv = H;
+      g.sA1 = (int64_t)H * S * S;
+      g.sA2 = (int64_t)S * S;
+      g.sB1 = (int64_t)S * 3 * h;
+      g.sB2 = HEAD_DIM;
+      g.sC1 = (int64_t)S * 3 * h;
+      g.sC2 = HEAD_DIM;
+      SITE(DK_BWD, Gemm<T>::run(g, false, false, EPI_STORE, false, BH, st));
+    }
+    if ((r = col_sum<T>(s, SITE_BQKV_SUM, SITE_BQKV_RED, dQKV, 3 * h, gr[STAGE_B_QKV]))) return r;
+    // dW_qkv = dQKV^T X
+    if ((r = wgrad<T>(s, SITE_WQKV_WGRAD, SITE_WQKV_RED, dQKV, 3 * h, (const T*)v.X, h, 3 * h, h, Tn, gr[STAGE_W_QKV]))) return r;
+    // dX = dZ1 + dQKV W_qkv  (the previous layer's dY, or the stage's dx)
+    T* dXout = (l > 0) ? (T*)s->dY : dx;
+    {
+      GemmArgs g = gemm_args(dQKV, 3 * h, p[STAGE_W_QKV], h, dXout, h, Tn, h, 3 * h);
+      g.aux = dZ1;
+      g.ldaux = h;
+      SITE(QKV_DGRAD, Gemm<T>::run(g, true, false, EPI_RESID, false, 1, st));
+    }
+    dYcur = dXout;
+  }
+  return STAGE_OK;
+}
+
+stage_status check_layer(stage_t* s, int layer, int which, int nwhich) {
+  if (!s) return STAGE_EINVAL;
+  if (layer < 0 || layer >= s->L) return fail(s, STAGE_EINVAL, "layer index out of range");
+  if (which < 0 || which >= nwhich) return fail(s, STAGE_EINVAL, "tensor index out of range");
+  return STAGE_OK;
+}
+
+}  // namespace
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+extern "C" {
+
+stage_status stage_init(int L, int hidden, int heads, int ffn, uint64_t seed, stage_dtype dtype,
+                        void* hip_stream, stage_t** out) {
+  if (!out) return STAGE_EINVAL;
+  *out = nullptr;
+  if (L < 1 || hidden < 64 || hidden % 64 || hidden > 2048 || heads < 1 || hidden % heads ||
+      hidden / heads != HEAD_DIM || ffn < 64 || ffn % 64 ||
+      (dtype != STAGE_F32 && dtype != STAGE_BF16))
+    return STAGE_EINVAL;
+  stage_t* s = new (std::nothrow) stage_t();
+  if (!s) return STAGE_ENOMEM;
+  s->L = L;
+  s->h = hidden;
+  s->H = heads;
+  s->f = ffn;
+  s->dtype = dtype;
+  s->esz = dtype == STAGE_BF16 ? 2 : 4;
+  s->stream = (hipStream_t)hip_stream;
+  s->param.resize(L);
+  s->grad.resize(L);
+  for (int l = 0; l < L; ++l) {
+    for (int w = 0; w < STAGE_NPARAM; ++w) {
+      int64_t n = param_numel(s, w);
+      stage_status st = dev_alloc(s, s->allocs, &s->param[l][w], n * param_esz(s, w));
+      if (!st) st = dev_alloc(s, s->allocs, (void**)&s->grad[l][w], n * 4);
+      if (st) {
+        for (void* p : s->allocs) (void)hipFree(p);
+        delete s;
+        return st;
+      }
+      const int blocks = (int)((n + 255) / 256);
+      if (is_matrix(w)) {
+        uint64_t key = splitmix64_mix(seed ^ ((uint64_t)(l * STAGE_NPARAM + w + 1) * GOLDEN));
+        if (dtype == STAGE_BF16)
+          hipLaunchKernelGGL(init_normal_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s->stream,
+                             (bf16_t*)s->param[l][w], n, key, 0.02);
+        else
+          hipLaunchKernelGGL(init_normal_kernel<float>, dim3(blocks), dim3(256), 0, s->stream,
+                             (float*)s->param[l][w], n, key, 0.02);
+      } else {
+        float v = (w == STAGE_G1 || w == STAGE_G2) ? 1.0f : 0.0f;
+        hipLaunchKernelGGL(fill_kernel, dim3(blocks), dim3(256), 0, s->stream,
+                           (float*)s->param[l][w], n, v);
+      }
+      hipLaunchKernelGGL(fill_kernel, dim3(blocks), dim3(256), 0, s->stream, s->grad[l][w], n,
+                         0.0f);
+    }
+  }
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
+  if (e != hipSuccess) {
+    for (void* p : s->allocs) (void)hipFree(p);
+    delete s;
+    return STAGE_EHIP;
+  }
+  *out = s;
+  return STAGE_OK;
+}
+
+stage_status stage_set_stream(stage_t* s, void* hip_stream) {
+  if (!s) return STAGE_EINVAL;
+  s->stream = (hipStream_t)hip_stream;
+  return STAGE_OK;
+}
+
+stage_status stage_forward(stage_t* s, const void* x, const uint8_t* key_mask, int batch, int seq,
+                           void* y) {
+  if (!s) return STAGE_EINVAL;
+  s->err.clear();
+  if (batch < 0 || seq < 0) return fail(s, STAGE_EINVAL, "negative batch or seq");
+  const int64_t T = (int64_t)batch * seq;
+  if (T > 0 && (!x || !y)) return fail(s, STAGE_EINVAL, "null x or y");
+  if (T > 0 && x == y) return fail(s, STAGE_EINVAL, "x and y may not alias");
+  if (T * std::max(3 * s->h, s->f) >= (int64_t)1 << 31)
+    return fail(s, STAGE_EINVAL, "batch * seq too large");
+  if (s->dtype == STAGE_BF16 && seq % 8 != 0)
+    return fail(s, STAGE_EINVAL, "bf16 stages need seq to be a multiple of 8");
+  if ((int64_t)batch * s->H * seq * seq >= (int64_t)1 << 40)
+    return fail(s, STAGE_EINVAL, "score matrix too large");
+  stage_status st = ensure_activations(s, batch, seq);
+  if (st) return st;
+  s->B = batch;
+  s->S = seq;
+  s->have_ctx = false;
+  if (T == 0) {
+    s->have_ctx = true;
+    return STAGE_OK;
+  }
+  if (key_mask) {
+    HIPCK(hipMemcpyAsync(s->mask, key_mask, (size_t)T, hipMemcpyDeviceToDevice, s->stream));
+  } else {
+    hipLaunchKernelGGL(ones_u8_kernel, dim3((unsigned)((T + 255) / 256)), dim3(256), 0, s->stream,
+                       s->mask, T);
+    HIPCK(hipGetLastError());
+  }
+  st = s->dtype == STAGE_BF16 ? forward_impl<bf16_t>(s, (const bf16_t*)x, (bf16_t*)y)
+                              : forward_impl<float>(s, (const float*)x, (float*)y);
+  if (st) return st;
+  s->have_ctx = true;
+  return STAGE_OK;
+}
+
+stage_status stage_backward(stage_t* s, const void* dy, void* dx) {
+  if (!s) return STAGE_EINVAL;
+  s->err.clear();
+  if (!s->have_ctx) return fail(s, STAGE_ESTATE, "stage_backward needs a preceding stage_forward");
+  const int64_t T = (int64_t)s->B * s->S;
+  if (T > 0 && (!dy || !dx)) return fail(s, STAGE_EINVAL, "null dy or dx");
+  s->have_ctx = false;
+  if (T == 0) {
+    for (int l = 0; l < s->L; ++l)
+      for (int w = 0; w < STAGE_NPARAM; ++w) {
+        int64_t n = param_numel(s, w);
+        hipLaunchKernelGGL(fill_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
+                           s->stream, s->grad[l][w], n, 0.0f);
+      }
+    HIPCK(hipGetLastError());
+    return STAGE_OK;
+  }
+  return s->dtype == STAGE_BF16 ? backward_impl<bf16_t>(s, (const bf16_t*)dy, (bf16_t*)dx)
+                                : backward_impl<float>(s, (const float*)dy, (float*)dx);
+}
+
+stage_status stage_param(stage_t* s, int layer, int which, void** dev_ptr, int64_t* numel,
+                         stage_dtype* dtype) {
+  stage_status st = check_layer(s, layer, which, STAGE_NPARAM);
+  if (st) return st;
+  if (dev_ptr) *dev_ptr = s->param[layer][which];
+  if (numel) *numel = param_numel(s, which);
+  if (dtype) *dtype = is_matrix(which) ? s->dtype : STAGE_F32;
+  return STAGE_OK;
+}
+
+stage_status stage_grad(stage_t* s, int layer, int which, float** dev_ptr, int64_t* numel) {
+  stage_status st = check_layer(s, layer, which, STAGE_NPARAM);
+  if (st) return st;
+  if (dev_ptr) *dev_ptr = s->grad[layer][which];
+  if (numel) *numel = param_numel(s, which);
+  return STAGE_OK;
+}
+
+stage_status stage_set_param(stage_t* s, int layer, int which, const void* src, size_t bytes) {
+  stage_status st = check_layer(s, layer, which, STAGE_NPARAM);
+  if (st) return st;
+  if (!src) return fail(s, STAGE_EINVAL, "null src");
+  size_t want = (size_t)param_numel(s, which) * param_esz(s, which);
+  if (bytes != want) return fail(s, STAGE_EINVAL, "byte count does not match the parameter");
+  HIPCK(hipMemcpyAsync(s->param[layer][which], src, bytes, hipMemcpyDefault, s->stream));
+  HIPCK(hipStreamSynchronize(s->stream));
+  return STAGE_OK;
+}
+
+static void* saved_ptr(stage_t* s, int layer, int which, size_t* bytes) {
+  const int64_t T = (int64_t)s->B * s->S;
+  const Saved& v = s->saved[layer];
+  const size_t e = s->esz;
+  switch (which) {
+    case STAGE_SAVED_X: *bytes = T * s->h * e; return v.X;
+    case STAGE_SAVED_QKV: *bytes = T * 3 * s->h * e; return v.QKV;
+    case STAGE_SAVED_CTX: *bytes = T * s->h * e; return v.C;
+    case STAGE_SAVED_H1: *bytes = T * s->h * e; return v.H1;
+    case STAGE_SAVED_U: *bytes = T * s->f * e; return v.U;
+    case STAGE_SAVED_G: *bytes = T * s->f * e; return v.G;
+  }
+  *bytes = 0;
+  return nullptr;
+}
+
+size_t stage_tensor_bytes(stage_t* s, int kind, int layer, int which) {
+  if (!s || layer < 0 || layer >= s->L) return 0;
+  if (kind == 0 && which >= 0 && which < STAGE_NPARAM)
+    return (size_t)param_numel(s, which) * param_esz(s, which);
+  if (kind == 1 && which >= 0 && which < STAGE_NPARAM) return (size_t)param_numel(s, which) * 4;
+  if (kind == 2 && which >= 0 && which < STAGE_NSAVED && (int)s->saved.size() == s->L) {
+    size_t b;
+    saved_ptr(s, layer, which, &b);
+    return b;
+  }
+  return 0;
+}
+
+stage_status stage_read(stage_t* s, int kind, int layer, int which, void* dst, size_t bytes) {
+  if (!s) return STAGE_EINVAL;
+  if (!dst) return fail(s, STAGE_EINVAL, "null dst");
+  const void* src = nullptr;
+  size_t want = 0;
+  if (kind == 0 || kind == 1) {
+    stage_status st = check_layer(s, layer, which, STAGE_NPARAM);
+    if (st) return st;
+    src = kind == 0 ? s->param[layer][which] : (const void*)s->grad[layer][which];
+    want = (size_t)param_numel(s, which) * (kind == 0 ? param_esz(s, which) : 4);
+  } else if (kind == 2) {
+    stage_status st = check_layer(s, layer, which, STAGE_NSAVED);
+    if (st) return st;
+    if ((int)s->saved.size() != s->L) return fail(s, STAGE_ESTATE, "no saved activations");
+    src = saved_ptr(s, layer, which, &want);
+  } else {
+    return fail(s, STAGE_EINVAL, "kind must be 0 (param), 1 (grad) or 2 (saved)");
+  }
+  if (bytes != want) return fail(s, STAGE_EINVAL, "byte count does not match the tensor");
+  if (want == 0) return STAGE_OK;
+  HIPCK(hipMemcpyAsync(dst, src, want, hipMemcpyDefault, s->stream));
+  HIPCK(hipStreamSynchronize(s->stream));
+  return STAGE_OK;
+}
+
+stage_status stage_trace_site(stage_t* s, int site) {
+  if (!s) return STAGE_EINVAL;
+  if (site < -1 || site >= SITE_COUNT) return fail(s, STAGE_EINVAL, "unknown site");
+  s->trace_site = site;
+  s->events_used = 0;
+  return STAGE_OK;
+}
+
+stage_status stage_trace_read(stage_t* s, int* launches, double* total_ms) {
+  if (!s) return STAGE_EINVAL;
+  HIPCK(hipStreamSynchronize(s->stream));
+  double tot = 0.0;
+  int n = 0;
+  for (size_t i = 0; i + 1 < s->events_used; i += 2) {
+    float ms = 0.0f;
+    HIPCK(hipEventElapsedTime(&ms, s->events[i], s->events[i + 1]));
+    tot += ms;
+    ++n;
+  }
+  s->events_used = 0;
+  if (launches) *launches = n;
+  if (total_ms) *total_ms = tot;
+  return STAGE_OK;
+}
+
+int stage_site_count(void) { return SITE_COUNT; }
+
+const char* stage_site_name(int site) {
+  return (site >= 0 && site < SITE_COUNT) ? SITE_NAMES[site] : "";
+}
+
+const char* stage_last_error(const stage_t* s) { return s ? s->err.c_str() : "null handle"; }
+
+void stage_destroy(stage_t* s) {
+  if (!s) return;
+  (void)hipStreamSynchronize(s->stream);
+  free_activations(s);
+  for (void* p : s->allocs) (void)hipFree(p);
+  for (hipEvent_t e : s->events) (void)hipEventDestroy(e);
+  delete s;
+}
+
+}  // extern "C"

@@ -1,0 +1,63 @@
+"""CPU-side checks of the boundary: the built library loads without a GPU and
+exports every function include/stage.h declares; the binding declares the
+same set; no product module imports the oracle."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "stage.h")
+LIB = os.path.join(ROOT, "paper_2202_11836_amd", "libskystage.so")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(stage_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_stage_calls():
+    names = declared_functions()
+    for n in ("stage_init", "stage_forward", "stage_backward", "stage_param", "stage_grad",
+              "stage_destroy", "stage_last_error"):
+        assert n in names
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="library not built (run __graft_entry__.build())")
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(LIB)
+    for n in declared_functions():
+        assert hasattr(lib, n), n
+
+
+def test_binding_covers_every_declared_symbol():
+    from paper_2202_11836_amd import binding
+    assert sorted(binding.EXPORTED) == declared_functions()
+
+
+def test_product_path_does_not_import_oracle():
+    pkg = os.path.join(ROOT, "paper_2202_11836_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                txt = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"^\s*(import|from)\s+oracle\b", txt, flags=re.M), f
+                assert "oracle/" not in txt, f
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    from paper_2202_11836_amd import binding
+    with pytest.raises(RuntimeError):
+        binding.load_library.__wrapped__(str(tmp_path / "nope.so")) if hasattr(binding.load_library, "__wrapped__") \
+            else _load_fresh(binding, str(tmp_path / "nope.so"))
+
+
+def _load_fresh(binding, path):
+    saved = binding._lib
+    binding._lib = None
+    try:
+        binding.load_library(path)
+    finally:
+        binding._lib = saved

@@ -1,0 +1,162 @@
+"""Contract of the C ABI on the GPU: error codes, state handling, empty
+batches, determinism, initialisation and partition invariance (re-splitting
+a block of layers into two chained stages must not change the result, the
+premise of re-allocating layers between devices, section III / IV-D)."""
+import numpy as np
+import pytest
+
+import synth
+from _parity import IDX, make_stage, to_numpy, to_torch
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def test_init_rejects_bad_dims():
+    from paper_2202_11836_amd import STAGE_BF16, StageError, stage_init
+    for args in [(0, 128, 2, 512), (1, 100, 2, 512), (1, 128, 3, 512), (1, 256, 2, 512),
+                 (1, 128, 2, 500), (1, 4096, 64, 512)]:
+        with pytest.raises(StageError):
+            stage_init(*args, 0, STAGE_BF16)
+
+
+def test_forward_backward_state_errors():
+    import torch
+    from paper_2202_11836_amd import Stage, StageError
+    _say("case abi state errors")
+    st = Stage(1, 128, 2, 256, seed=1, dtype="bf16")
+    dy = torch.zeros(2, 16, 128, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(StageError) as e:
+        st.backward(dy)
+    assert e.value.status == 2
+    x = torch.randn(2, 16, 128, device="cuda").to(torch.bfloat16)
+    st.forward(x)
+    st.backward(dy)
+    with pytest.raises(StageError) as e:  # context consumed
+        st.backward(dy)
+    assert e.value.status == 2
+    with pytest.raises(StageError) as e:  # bf16 seq must be a multiple of 8
+        st.forward(torch.zeros(2, 13, 128, dtype=torch.bfloat16, device="cuda"))
+    assert e.value.status == 1
+    with pytest.raises(StageError):
+        st.param(1, 0)
+    with pytest.raises(StageError):
+        st.param(0, 12)
+    st.close()
+
+
+def test_empty_batch():
+    import torch
+    from paper_2202_11836_amd import Stage
+    st = Stage(2, 128, 2, 256, seed=1, dtype="f32")
+    x = torch.zeros(0, 8, 128, device="cuda")
+    y = st.forward(x)
+    dx = st.backward(torch.zeros_like(x))
+    torch.cuda.synchronize()
+    assert y.shape == (0, 8, 128) and dx.shape == (0, 8, 128)
+    for l in range(2):
+        for w in range(12):
+            assert float(st.grad(l, w).abs().max()) == 0.0
+    st.close()
+
+
+def test_init_statistics_and_seed_determinism():
+    from paper_2202_11836_amd import Stage
+    a = Stage(2, 256, 4, 1024, seed=7, dtype="bf16")
+    b = Stage(2, 256, 4, 1024, seed=7, dtype="bf16")
+    c = Stage(2, 256, 4, 1024, seed=8, dtype="bf16")
+    for l in range(2):
+        for w in range(12):
+            pa = to_numpy(a.param(l, w))
+            pb = to_numpy(b.param(l, w))
+            np.testing.assert_array_equal(pa, pb)
+            if w in (0, 2, 6, 8):
+                assert abs(pa.mean()) < 2e-3 and abs(pa.std() - 0.02) < 1e-3
+                assert not np.array_equal(pa, to_numpy(c.param(l, w)))
+            elif w in (4, 10):
+                assert np.all(pa == 1.0)
+            else:
+                assert np.all(pa == 0.0)
+    # distinct layers / tensors get distinct streams
+    assert not np.array_equal(to_numpy(a.param(0, 2)), to_numpy(a.param(1, 2)))
+    for s in (a, b, c):
+        s.close()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_bitwise_determinism(dtype):
+    import torch
+    cfg = synth.StageConfig("det", 2, 256, 4, 512, 4, 64, 10, 64, dtype, 5)
+    _say(f"case determinism {dtype}")
+    inp = synth.make_inputs(cfg)
+    params = synth.make_params(cfg, perturb=True)
+    st = make_stage(cfg, params)
+    x = to_torch(inp["x"], dtype)
+    mask = torch.from_numpy(inp["mask"]).cuda()
+    dy = to_torch(inp["dy"], dtype)
+    outs = []
+    for _ in range(2):
+        y = st.forward(x, mask)
+        dx = st.backward(dy)
+        torch.cuda.synchronize()
+        outs.append((y.clone(), dx.clone(), [st.grad(l, w) for l in range(2) for w in range(12)]))
+    assert torch.equal(outs[0][0], outs[1][0])
+    assert torch.equal(outs[0][1], outs[1][1])
+    for g0, g1 in zip(outs[0][2], outs[1][2]):
+        assert torch.equal(g0, g1)
+    st.close()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_partition_invariance(dtype):
+    """Layers [0,3) as one stage == stage [0,1) then stage [1,3), chained
+    through y -> x forward and dx -> dy backward (bitwise)."""
+    import torch
+    cfg = synth.StageConfig("part", 3, 128, 2, 256, 2, 32, 8, 32, dtype, 9)
+    _say(f"case partition {dtype}")
+    inp = synth.make_inputs(cfg)
+    params = synth.make_params(cfg, perturb=True)
+    whole = make_stage(cfg, params)
+    first = make_stage(cfg.with_(L=1), params[:1])
+    second = make_stage(cfg.with_(L=2), params[1:])
+    x = to_torch(inp["x"], dtype)
+    mask = torch.from_numpy(inp["mask"]).cuda()
+    dy = to_torch(inp["dy"], dtype)
+    y = whole.forward(x, mask)
+    dx = whole.backward(dy)
+    y1 = first.forward(x, mask)
+    y2 = second.forward(y1, mask)
+    d1 = second.backward(dy)
+    d0 = first.backward(d1)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
+    assert torch.equal(dx, d0)
+    for w in range(12):
+        assert torch.equal(whole.grad(0, w), first.grad(0, w))
+        assert torch.equal(whole.grad(1, w), second.grad(0, w))
+        assert torch.equal(whole.grad(2, w), second.grad(1, w))
+    for s in (whole, first, second):
+        s.close()
+
+
+def test_stream_is_respected():
+    """Work enqueued on a side stream is ordered on that stream."""
+    import torch
+    cfg = synth.StageConfig("strm", 1, 128, 2, 256, 2, 32, None, None, "bf16", 4)
+    inp = synth.make_inputs(cfg)
+    params = synth.make_params(cfg)
+    st = make_stage(cfg, params)
+    x = to_torch(inp["x"], "bf16")
+    ref = st.forward(x)
+    st.backward(to_torch(inp["dy"], "bf16"))
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        y = st.forward(x)
+        st.backward(to_torch(inp["dy"], "bf16"))
+    side.synchronize()
+    assert torch.equal(y, ref)
+    st.close()
