@@ -155,7 +155,8 @@ stage_status stage_trace_read(stage_t* s, int* launches, double* total_ms);
 int stage_site_count(void);
 const char* stage_site_name(int site); /* "" for an unknown site */
 
-/* Message describing the last failure on this handle ("" if none). */
+/* Message describing the last failure on this handle ("" if none); with
+ * s == NULL, the message of the last failed stage_init on this thread. */
 const char* stage_last_error(const stage_t* s);
 
 /* Free everything the handle owns (synchronises its stream). NULL is a no-op. */

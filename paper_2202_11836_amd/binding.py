@@ -43,6 +43,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is not built; run __graft_entry__.build() first")
+    # torch ships its own HIP runtime (same soname as /opt/rocm's).  Load it
+    # first so that the library binds to the runtime that owns torch's
+    # device memory and streams, never to a second copy in the process.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     vp, i32, i64, u64, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_uint64, ctypes.c_size_t
     lib.stage_init.argtypes = [i32, i32, i32, i32, u64, i32, vp, ctypes.POINTER(vp)]
@@ -108,7 +112,7 @@ def stage_init(L: int, hidden: int, heads: int, ffn: int, seed: int, dtype: int,
     st = lib.stage_init(L, hidden, heads, ffn, seed, dtype,
                         stream if stream is not None else _current_stream(), ctypes.byref(out))
     if st != STAGE_OK:
-        raise StageError(st, "stage_init rejected the arguments or failed")
+        raise StageError(st, "stage_init: " + (lib.stage_last_error(None) or b"").decode())
     return out
 
 

@@ -62,17 +62,22 @@ hipError_t splitk_reduce(const float* part, int splits, int M, int N, float* out
 // Row kernels (one wavefront per row), T = float or bf16_t.
 // ---------------------------------------------------------------------------
 // z = a + bias + resid;  y = gamma * xhat + beta with xhat = (z - mean) * rstd.
-template <typename T>
-hipError_t add_ln_fwd(const T* a, const float* bias, const T* resid, const float* gamma,
-                      const float* beta, T* y, T* xhat, float* rstd, int rows, int h,
+// a is the fp32 output of the preceding GEMM; y32 (optional, may be null)
+// receives y in fp32 as well.
+template <typename T, typename TA, typename TR>
+hipError_t add_ln_fwd(const TA* a, const float* bias, const TR* resid, const float* gamma,
+                      const float* beta, T* y, float* y32, T* xhat, float* rstd, int rows, int h,
                       hipStream_t st);
 
 // dz = rstd * (g - mean(g) - xhat * mean(g * xhat)), g = dy * gamma.
-// Column partial sums per row block: part[blk][0][:] = sum dy*xhat,
-// part[blk][1][:] = sum dy, part[blk][2][:] = sum dz.
+// Column partial sums per block of LN_BWD_RPB rows (ln_bwd_blocks(rows)
+// blocks): part[blk][0][:] = sum dy*xhat, part[blk][1][:] = sum dy,
+// part[blk][2][:] = sum dz.
+constexpr int LN_BWD_RPB = 16;
+int ln_bwd_blocks(int rows);
 template <typename T>
 hipError_t ln_bwd(const T* dy, const T* xhat, const float* rstd, const float* gamma, T* dz,
-                  float* part, int nblk, int rows, int h, hipStream_t st);
+                  float* part, int rows, int h, hipStream_t st);
 
 // part[blk][n] = sum over the block's rows of x[row][n].
 template <typename T>

@@ -8,117 +8,204 @@
 namespace {
 
 constexpr float LN_EPS = 1e-12f;
-constexpr int MAXV = 32;  // columns per lane: rows of up to 64 * 32 = 2048
 
-template <typename T>
-__global__ __launch_bounds__(256) void add_ln_fwd_kernel(const T* __restrict__ a,
+// 8 consecutive elements <-> 8 floats (16-byte bf16 / 32-byte fp32 accesses).
+__device__ __forceinline__ void load8(const bf16_t* p, float v[8]) {
+  u32x4_t r = *(const u32x4_t*)p;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __uint_as_float(r[i] << 16);
+    v[2 * i + 1] = __uint_as_float(r[i] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ void load8(const float* p, float v[8]) {
+  f32x4_t a = *(const f32x4_t*)p, b = *(const f32x4_t*)(p + 4);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[i] = a[i];
+    v[4 + i] = b[i];
+  }
+}
+__device__ __forceinline__ void store8(bf16_t* p, const float v[8]) {
+  u32x4_t r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) r[i] = (uint32_t)f2bf(v[2 * i]) | ((uint32_t)f2bf(v[2 * i + 1]) << 16);
+  *(u32x4_t*)p = r;
+}
+__device__ __forceinline__ void store8(float* p, const float v[8]) {
+  f32x4_t a, b;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    a[i] = v[i];
+    b[i] = v[4 + i];
+  }
+  *(f32x4_t*)p = a;
+  *(f32x4_t*)(p + 4) = b;
+}
+// Round to the storage type and back (what a store followed by a load gives).
+__device__ __forceinline__ float as_stored(float v, const bf16_t*) { return bf2f(f2bf(v)); }
+__device__ __forceinline__ float as_stored(float v, const float*) { return v; }
+
+// One wavefront per row.  Lane `lane` owns the 8-column chunks
+// c = lane + 64 i (i < NC, c < h / 8).
+template <typename T, typename TA, typename TR, int NC>
+__global__ __launch_bounds__(256) void add_ln_fwd_kernel(const TA* __restrict__ a,
                                                          const float* __restrict__ bias,
-                                                         const T* __restrict__ resid,
+                                                         const TR* __restrict__ resid,
                                                          const float* __restrict__ gamma,
                                                          const float* __restrict__ beta,
-                                                         T* __restrict__ y, T* __restrict__ xhat,
+                                                         T* __restrict__ y, float* __restrict__ y32,
+                                                         T* __restrict__ xhat,
                                                          float* __restrict__ rstd, int rows, int h) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= rows) return;
-  const int nv = h >> 6;
+  const int nchunk = h >> 3;
   const int64_t base = (int64_t)row * h;
-  float z[MAXV];
+  float z[NC][8];
   float s = 0.0f;
 #pragma unroll
-  for (int i = 0; i < MAXV; ++i) {
-    if (i < nv) {
-      int c = lane + 64 * i;
-      z[i] = ld_f(a + base + c) + bias[c] + ld_f(resid + base + c);
-      s += z[i];
+  for (int i = 0; i < NC; ++i) {
+    const int c = lane + 64 * i;
+    if (c < nchunk) {
+      float av[8], rv[8], bv[8];
+      load8(a + base + 8 * c, av);
+      load8(resid + base + 8 * c, rv);
+      load8(bias + 8 * c, bv);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        z[i][k] = av[k] + bv[k] + rv[k];
+        s += z[i][k];
+      }
     }
   }
   const float mean = wave_sum(s) / (float)h;
   float s2 = 0.0f;
 #pragma unroll
-  for (int i = 0; i < MAXV; ++i) {
-    if (i < nv) {
-      float d = z[i] - mean;
-      s2 += d * d;
+  for (int i = 0; i < NC; ++i) {
+    if (lane + 64 * i < nchunk) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        float d = z[i][k] - mean;
+        s2 += d * d;
+      }
     }
   }
   const float var = wave_sum(s2) / (float)h;
   const float r = 1.0f / sqrtf(var + LN_EPS);
 #pragma unroll
-  for (int i = 0; i < MAXV; ++i) {
-    if (i < nv) {
-      int c = lane + 64 * i;
-      float xh = (z[i] - mean) * r;
-      st_f(xhat + base + c, xh);
-      st_f(y + base + c, gamma[c] * xh + beta[c]);
+  for (int i = 0; i < NC; ++i) {
+    const int c = lane + 64 * i;
+    if (c < nchunk) {
+      float gv[8], btv[8], xh[8], yv[8];
+      load8(gamma + 8 * c, gv);
+      load8(beta + 8 * c, btv);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        xh[k] = (z[i][k] - mean) * r;
+        yv[k] = gv[k] * xh[k] + btv[k];
+      }
+      store8(xhat + base + 8 * c, xh);
+      store8(y + base + 8 * c, yv);
+      if (y32) store8(y32 + base + 8 * c, yv);
     }
   }
   if (lane == 0) rstd[row] = r;
 }
 
-// Each wavefront walks its rows and keeps per-column partial sums in
-// registers; partials are written per wavefront (no atomics) and summed in a
-// fixed order by col_reduce.
-template <typename T>
+// LayerNorm backward.  A block of 4 wavefronts handles `rpb` consecutive
+// rows (one row per wavefront at a time); per-column partial sums of
+// dy*xhat, dy and dz are kept per lane, combined across the 4 wavefronts in
+// LDS in a fixed order and written as one partial row per block.
+template <typename T, int NC>
 __global__ __launch_bounds__(256) void ln_bwd_kernel(const T* __restrict__ dy,
                                                      const T* __restrict__ xhat,
                                                      const float* __restrict__ rstd,
                                                      const float* __restrict__ gamma,
                                                      T* __restrict__ dz, float* __restrict__ part,
-                                                     int rows, int h, int rows_per_wave) {
-  const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
+                                                     int rows, int h, int rpb) {
+  extern __shared__ float red[];  // [3][h]
+  const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
-  const int nv = h >> 6;
-  float pg[MAXV], pb[MAXV], pz[MAXV];
+  const int nchunk = h >> 3;
+  float pg[NC][8], pb[NC][8], pz[NC][8], gm[NC][8];
 #pragma unroll
-  for (int i = 0; i < MAXV; ++i) pg[i] = pb[i] = pz[i] = 0.0f;
-  const int r0 = wid * rows_per_wave;
-  const int r1 = min(rows, r0 + rows_per_wave);
+  for (int i = 0; i < NC; ++i) {
+    const int c = lane + 64 * i;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) pg[i][k] = pb[i][k] = pz[i][k] = 0.0f;
+    if (c < nchunk) load8(gamma + 8 * c, gm[i]);
+  }
+  const int r0 = blockIdx.x * rpb;
+  const int r1 = min(rows, r0 + rpb);
   const float inv_h = 1.0f / (float)h;
-  for (int row = r0; row < r1; ++row) {
+  for (int row = r0 + wave; row < r1; row += 4) {
     const int64_t base = (int64_t)row * h;
-    float dyv[MAXV], xv[MAXV];
+    float dv[NC][8], xv[NC][8];
     float sg = 0.0f, sgx = 0.0f;
 #pragma unroll
-    for (int i = 0; i < MAXV; ++i) {
-      if (i < nv) {
-        int c = lane + 64 * i;
-        dyv[i] = ld_f(dy + base + c);
-        xv[i] = ld_f(xhat + base + c);
-        float g = dyv[i] * gamma[c];
-        sg += g;
-        sgx += g * xv[i];
-        pg[i] += dyv[i] * xv[i];
-        pb[i] += dyv[i];
+    for (int i = 0; i < NC; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nchunk) {
+        load8(dy + base + 8 * c, dv[i]);
+        load8(xhat + base + 8 * c, xv[i]);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          float g = dv[i][k] * gm[i][k];
+          sg += g;
+          sgx += g * xv[i][k];
+          pg[i][k] += dv[i][k] * xv[i][k];
+          pb[i][k] += dv[i][k];
+        }
       }
     }
     sg = wave_sum(sg) * inv_h;
     sgx = wave_sum(sgx) * inv_h;
     const float r = rstd[row];
 #pragma unroll
-    for (int i = 0; i < MAXV; ++i) {
-      if (i < nv) {
-        int c = lane + 64 * i;
-        float d = r * (dyv[i] * gamma[c] - sg - xv[i] * sgx);
-        T dq;
-        st_f(&dq, d);
-        dz[base + c] = dq;
-        // The column sum uses the value as stored, so that the bias gradient
-        // of the preceding linear layer matches the gradient that flows on.
-        pz[i] += ld_f(&dq);
+    for (int i = 0; i < NC; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nchunk) {
+        float d[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          d[k] = r * (dv[i][k] * gm[i][k] - sg - xv[i][k] * sgx);
+          // The column sum uses the value as stored, so that the bias
+          // gradient of the preceding linear layer matches the gradient
+          // that flows on.
+          pz[i][k] += as_stored(d[k], dz);
+        }
+        store8(dz + base + 8 * c, d);
       }
     }
   }
-  float* P = part + (int64_t)wid * 3 * h;
+  // Fixed-order combination of the 4 wavefronts' partials.
+  for (int w = 0; w < 4; ++w) {
+    if (wave == w) {
 #pragma unroll
-  for (int i = 0; i < MAXV; ++i) {
-    if (i < nv) {
-      int c = lane + 64 * i;
-      P[c] = pg[i];
-      P[h + c] = pb[i];
-      P[2 * h + c] = pz[i];
+      for (int i = 0; i < NC; ++i) {
+        const int c = lane + 64 * i;
+        if (c < nchunk) {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) {
+            const int col = 8 * c + k;
+            if (w == 0) {
+              red[col] = pg[i][k];
+              red[h + col] = pb[i][k];
+              red[2 * h + col] = pz[i][k];
+            } else {
+              red[col] += pg[i][k];
+              red[h + col] += pb[i][k];
+              red[2 * h + col] += pz[i][k];
+            }
+          }
+        }
+      }
     }
+    __syncthreads();
   }
+  float* P = part + (int64_t)blockIdx.x * 3 * h;
+  for (int e = threadIdx.x; e < 3 * h; e += 256) P[e] = red[e];
 }
 
 template <typename T>
@@ -138,14 +225,24 @@ struct OutPtrs {
   float* p[4];
 };
 
-__global__ __launch_bounds__(256) void col_reduce_kernel(const float* __restrict__ part, int nblk,
-                                                         int nvec, int n, OutPtrs outs) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
+// 64 columns x 16 stripes of partial rows per block; the 16 stripe sums are
+// combined in LDS by a fixed-order tree.
+__global__ __launch_bounds__(1024) void col_reduce_kernel(const float* __restrict__ part, int nblk,
+                                                          int nvec, int n, OutPtrs outs) {
+  __shared__ float sm[16][65];
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + tx;
   const int v = blockIdx.y;
-  if (c >= n || v >= nvec) return;
   float s = 0.0f;
-  for (int b = 0; b < nblk; ++b) s += part[((int64_t)b * nvec + v) * n + c];
-  if (outs.p[v]) outs.p[v][c] = s;
+  if (c < n)
+    for (int b = ty; b < nblk; b += 16) s += part[((int64_t)b * nvec + v) * n + c];
+  sm[ty][tx] = s;
+  __syncthreads();
+  for (int w = 8; w > 0; w >>= 1) {
+    if (ty < w) sm[ty][tx] += sm[ty + w][tx];
+    __syncthreads();
+  }
+  if (ty == 0 && c < n && outs.p[v]) outs.p[v][c] = sm[0][tx];
 }
 
 // P = softmax over keys of scale * scores, masked keys -> 0, empty rows -> 0.
@@ -203,26 +300,44 @@ __global__ __launch_bounds__(256) void softmax_bwd_kernel(const float* __restric
 
 }  // namespace
 
-template <typename T>
-hipError_t add_ln_fwd(const T* a, const float* bias, const T* resid, const float* gamma,
-                      const float* beta, T* y, T* xhat, float* rstd, int rows, int h,
+template <typename T, typename TA, typename TR>
+hipError_t add_ln_fwd(const TA* a, const float* bias, const TR* resid, const float* gamma,
+                      const float* beta, T* y, float* y32, T* xhat, float* rstd, int rows, int h,
                       hipStream_t st) {
-  if (h % 64 != 0 || h > 64 * MAXV) return hipErrorInvalidValue;
+  if (h % 64 != 0 || h > 2048) return hipErrorInvalidValue;
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(add_ln_fwd_kernel<T>, dim3((rows + 3) / 4), dim3(256), 0, st, a, bias, resid,
-                     gamma, beta, y, xhat, rstd, rows, h);
+  const int nc = (h / 8 + 63) / 64;
+  dim3 grid((rows + 3) / 4), blk(256);
+#define LAUNCH_LN(NCV)                                                                        \
+  hipLaunchKernelGGL((add_ln_fwd_kernel<T, TA, TR, NCV>), grid, blk, 0, st, a, bias, resid, gamma, \
+                     beta, y, y32, xhat, rstd, rows, h)
+  switch (nc) {
+    case 1: LAUNCH_LN(1); break;
+    case 2: LAUNCH_LN(2); break;
+    case 3: LAUNCH_LN(3); break;
+    default: LAUNCH_LN(4); break;
+  }
+#undef LAUNCH_LN
   return hipGetLastError();
 }
 
+int ln_bwd_blocks(int rows) { return (rows + LN_BWD_RPB - 1) / LN_BWD_RPB; }
+
 template <typename T>
 hipError_t ln_bwd(const T* dy, const T* xhat, const float* rstd, const float* gamma, T* dz,
-                  float* part, int nblk, int rows, int h, hipStream_t st) {
-  // nblk counts wavefronts (partial rows of part); it must be a multiple of 4.
-  if (h % 64 != 0 || h > 64 * MAXV || nblk % 4 != 0) return hipErrorInvalidValue;
-  int rpw = (rows + nblk - 1) / nblk;
-  if (rpw < 1) rpw = 1;
-  hipLaunchKernelGGL(ln_bwd_kernel<T>, dim3(nblk / 4), dim3(256), 0, st, dy, xhat, rstd, gamma, dz,
-                     part, rows, h, rpw);
+                  float* part, int rows, int h, hipStream_t st) {
+  if (h % 64 != 0 || h > 2048) return hipErrorInvalidValue;
+  if (rows <= 0) return hipSuccess;
+  const int nc = (h / 8 + 63) / 64;
+  dim3 grid(ln_bwd_blocks(rows)), blk(256);
+  size_t sh = (size_t)3 * h * sizeof(float);
+  const int rpb = LN_BWD_RPB;
+  switch (nc) {
+    case 1: hipLaunchKernelGGL((ln_bwd_kernel<T, 1>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
+    case 2: hipLaunchKernelGGL((ln_bwd_kernel<T, 2>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
+    case 3: hipLaunchKernelGGL((ln_bwd_kernel<T, 3>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
+    default: hipLaunchKernelGGL((ln_bwd_kernel<T, 4>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
+  }
   return hipGetLastError();
 }
 
@@ -240,7 +355,7 @@ hipError_t col_reduce(const float* part, int nblk, int nvec, int n, float* const
   if (nvec > 4) return hipErrorInvalidValue;
   OutPtrs o{};
   for (int i = 0; i < nvec; ++i) o.p[i] = outs[i];
-  hipLaunchKernelGGL(col_reduce_kernel, dim3((n + 255) / 256, nvec), dim3(256), 0, st, part, nblk,
+  hipLaunchKernelGGL(col_reduce_kernel, dim3((n + 63) / 64, nvec), dim3(1024), 0, st, part, nblk,
                      nvec, n, o);
   return hipGetLastError();
 }
@@ -266,10 +381,11 @@ hipError_t softmax_bwd(const float* dP, const T* P, T* dS, int BH, int S, int ld
 }
 
 #define INST(T)                                                                                 \
-  template hipError_t add_ln_fwd<T>(const T*, const float*, const T*, const float*,            \
-                                    const float*, T*, T*, float*, int, int, hipStream_t);      \
+  template hipError_t add_ln_fwd<T, float, T>(const float*, const float*, const T*,            \
+                                              const float*, const float*, T*, float*, T*,     \
+                                              float*, int, int, hipStream_t);                 \
   template hipError_t ln_bwd<T>(const T*, const T*, const float*, const float*, T*, float*,    \
-                                int, int, int, hipStream_t);                                   \
+                                int, int, hipStream_t);                                        \
   template hipError_t col_partial<T>(const T*, int, int, float*, int, hipStream_t);            \
   template hipError_t softmax_fwd<T>(const float*, const uint8_t*, T*, int, int, int, int,     \
                                      float, hipStream_t);                                      \
@@ -277,3 +393,7 @@ hipError_t softmax_bwd(const float* dP, const T* P, T* dS, int BH, int S, int ld
                                      hipStream_t);
 INST(float)
 INST(bf16_t)
+template hipError_t add_ln_fwd<bf16_t, float, float>(const float*, const float*, const float*,
+                                                       const float*, const float*, bf16_t*,
+                                                       float*, bf16_t*, float*, int, int,
+                                                       hipStream_t);

@@ -11,6 +11,7 @@
 #include <cstring>
 #include <new>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "../../include/stage.h"
@@ -19,7 +20,6 @@
 namespace {
 
 constexpr int HEAD_DIM = 64;
-constexpr int LN_PARTS = 256;  // wavefront partials of the LayerNorm backward
 constexpr int COL_PARTS = 128; // row blocks of the bias-gradient column sums
 
 // Kernel launch sites of one layer, for event tracing (stage_trace_site).
@@ -119,7 +119,8 @@ struct stage {
   std::vector<void*> act_allocs;
   std::vector<Saved> saved;
   uint8_t* mask = nullptr;
-  void* tmp = nullptr;      // [T, h] GEMM output before LayerNorm
+  float* tmp = nullptr;     // [T, h] fp32 GEMM output before LayerNorm
+  float* h1f = nullptr;     // [T, h] fp32 copy of H1 (bf16 stages)
   float* scores = nullptr;  // [B*H, S, S] fp32 (scores, then dP)
   void* dS = nullptr;       // [B*H, S, S]
   void* dQKV = nullptr;     // [T, 3h]
@@ -144,6 +145,9 @@ struct stage {
 };
 
 namespace {
+
+// Message of the last failed stage_init on this thread (no handle exists).
+thread_local std::string g_init_err;
 
 stage_status fail(stage_t* s, stage_status st, const std::string& msg) {
   if (s) s->err = msg;
@@ -179,17 +183,17 @@ void trace_end(stage_t* s, int idx) {
   (void)hipEventRecord(s->events[idx + 1], s->stream);
 }
 
-// Launch expression `expr` (a hipError_t) as traced site number `site`.
-#define SITE_I(site, expr)                                                        \
+// Launch expression (a hipError_t) as traced site number `site`.
+#define SITE_I(site, ...)                                                         \
   do {                                                                            \
     int tr_ = trace_begin(s, (site));                                             \
-    hipError_t e_ = (expr);                                                       \
+    hipError_t e_ = (__VA_ARGS__);                                                \
     trace_end(s, tr_);                                                            \
     if (e_ != hipSuccess)                                                         \
       return fail(s, STAGE_EHIP,                                                  \
                   std::string(SITE_NAMES[(site)]) + ": " + hipGetErrorString(e_)); \
   } while (0)
-#define SITE(id, expr) SITE_I(SITE_##id, expr)
+#define SITE(id, ...) SITE_I(SITE_##id, __VA_ARGS__)
 
 int64_t param_numel(const stage_t* s, int which) {
   const int64_t h = s->h, f = s->f;
@@ -256,14 +260,16 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
         (st = A(&v.xhat2, T * h * e)) || (st = A((void**)&v.rstd2, T * 4)))
       return st;
   }
-  if ((st = A((void**)&s->mask, T)) || (st = A(&s->tmp, T * h * e)) ||
+  if ((st = A((void**)&s->mask, T)) || (st = A((void**)&s->tmp, T * h * 4)) ||
+      (st = A((void**)&s->h1f, T * h * 4)) ||
       (st = A((void**)&s->scores, BSS * 4)) || (st = A(&s->dS, BSS * e)) ||
       (st = A(&s->dQKV, T * 3 * h * e)) || (st = A(&s->dZ2, T * h * e)) ||
       (st = A(&s->dU, T * f * e)) || (st = A(&s->dH1, T * h * e)) ||
       (st = A(&s->dZ1, T * h * e)) || (st = A(&s->dC, T * h * e)) || (st = A(&s->dY, T * h * e)))
     return st;
   const int64_t maxw = std::max<int64_t>(3 * h, f);
-  const int64_t part_elems = std::max<int64_t>((int64_t)LN_PARTS * 3 * h, (int64_t)COL_PARTS * maxw);
+  const int64_t part_elems =
+      std::max<int64_t>((int64_t)ln_bwd_blocks((int)T) * 3 * h, (int64_t)COL_PARTS * maxw);
   if ((st = A((void**)&s->part, part_elems * 4))) return st;
   // Split-K partials: largest weight gradient times its split count.
   size_t need = 0;
@@ -362,14 +368,17 @@ stage_status forward_impl(stage_t* s, const T* x, T* y) {
       g.sC2 = HEAD_DIM;
       SITE(CTX_FWD, Gemm<T>::run(g, true, false, EPI_STORE, false, BH, st));
     }
-    // tmp = C W_o^T;  H1 = LN(X + tmp + b_o)
+    // tmp = C W_o^T (fp32);  H1 = LN(X + tmp + b_o)
     {
       GemmArgs g = gemm_args(v.C, h, p[STAGE_W_O], h, s->tmp, h, Tn, h, h);
-      SITE(OUT_FWD, Gemm<T>::run(g, true, true, EPI_STORE, false, 1, st));
+      SITE(OUT_FWD, Gemm<T>::run(g, true, true, EPI_STORE, true, 1, st));
     }
-    SITE(LN1_FWD, add_ln_fwd<T>((const T*)s->tmp, (const float*)p[STAGE_B_O], X,
-                        (const float*)p[STAGE_G1], (const float*)p[STAGE_BE1], (T*)v.H1,
-                        (T*)v.xhat1, v.rstd1, Tn, h, st));
+    // For bf16 stages H1 is also written in fp32: it is the residual of the
+    // second LayerNorm, so its rounding to bf16 stays out of Y.
+    float* h1_32 = std::is_same<T, float>::value ? nullptr : s->h1f;
+    SITE(LN1_FWD, add_ln_fwd<T, float, T>(s->tmp, (const float*)p[STAGE_B_O], X,
+                                   (const float*)p[STAGE_G1], (const float*)p[STAGE_BE1],
+                                   (T*)v.H1, h1_32, (T*)v.xhat1, v.rstd1, Tn, h, st));
     // U = H1 W_1^T + b_1;  G = GELU(U)
     {
       GemmArgs g = gemm_args(v.H1, h, p[STAGE_W_1], h, v.U, f, Tn, f, h);
@@ -377,15 +386,21 @@ stage_status forward_impl(stage_t* s, const T* x, T* y) {
       g.C2 = v.G;
       SITE(FFN1_FWD, Gemm<T>::run(g, true, true, EPI_GELU, false, 1, st));
     }
-    // tmp = G W_2^T;  Y = LN(H1 + tmp + b_2)
+    // tmp = G W_2^T (fp32);  Y = LN(H1 + tmp + b_2)
     {
       GemmArgs g = gemm_args(v.G, f, p[STAGE_W_2], f, s->tmp, h, Tn, h, f);
-      SITE(FFN2_FWD, Gemm<T>::run(g, true, true, EPI_STORE, false, 1, st));
+      SITE(FFN2_FWD, Gemm<T>::run(g, true, true, EPI_STORE, true, 1, st));
     }
     T* Y = (l + 1 < s->L) ? (T*)s->saved[l + 1].X : y;
-    SITE(LN2_FWD, add_ln_fwd<T>((const T*)s->tmp, (const float*)p[STAGE_B_2], (const T*)v.H1,
-                        (const float*)p[STAGE_G2], (const float*)p[STAGE_BE2], Y, (T*)v.xhat2,
-                        v.rstd2, Tn, h, st));
+    if (h1_32)
+      SITE(LN2_FWD, add_ln_fwd<T, float, float>(s->tmp, (const float*)p[STAGE_B_2], h1_32,
+                                         (const float*)p[STAGE_G2], (const float*)p[STAGE_BE2],
+                                         Y, nullptr, (T*)v.xhat2, v.rstd2, Tn, h, st));
+    else
+      SITE(LN2_FWD, add_ln_fwd<T, float, T>(s->tmp, (const float*)p[STAGE_B_2],
+                                     (const T*)v.H1, (const float*)p[STAGE_G2],
+                                     (const float*)p[STAGE_BE2], Y, nullptr, (T*)v.xhat2,
+                                     v.rstd2, Tn, h, st));
   }
   return STAGE_OK;
 }
@@ -394,9 +409,9 @@ template <typename T>
 stage_status ln_backward(stage_t* s, int site, int site_red, const T* dy, const T* xhat, const float* rstd,
                          const float* gamma, T* dz, float* dgamma, float* dbeta, float* dbias) {
   const int Tn = s->B * s->S, h = s->h;
-  SITE_I(site, ln_bwd<T>(dy, xhat, rstd, gamma, dz, s->part, LN_PARTS, Tn, h, s->stream));
+  SITE_I(site, ln_bwd<T>(dy, xhat, rstd, gamma, dz, s->part, Tn, h, s->stream));
   float* outs[3] = {dgamma, dbeta, dbias};
-  SITE_I(site_red, col_reduce(s->part, LN_PARTS, 3, h, outs, s->stream));
+  SITE_I(site_red, col_reduce(s->part, ln_bwd_blocks(Tn), 3, h, outs, s->stream));
   return STAGE_OK;
 }
 
@@ -545,12 +560,19 @@ extern "C" {
 
 stage_status stage_init(int L, int hidden, int heads, int ffn, uint64_t seed, stage_dtype dtype,
                         void* hip_stream, stage_t** out) {
-  if (!out) return STAGE_EINVAL;
+  g_init_err.clear();
+  if (!out) {
+    g_init_err = "null out";
+    return STAGE_EINVAL;
+  }
   *out = nullptr;
   if (L < 1 || hidden < 64 || hidden % 64 || hidden > 2048 || heads < 1 || hidden % heads ||
       hidden / heads != HEAD_DIM || ffn < 64 || ffn % 64 ||
-      (dtype != STAGE_F32 && dtype != STAGE_BF16))
+      (dtype != STAGE_F32 && dtype != STAGE_BF16)) {
+    g_init_err = "invalid dims: need L >= 1, hidden a multiple of 64 and <= 2048, "
+                 "hidden / heads == 64, ffn a multiple of 64";
     return STAGE_EINVAL;
+  }
   stage_t* s = new (std::nothrow) stage_t();
   if (!s) return STAGE_ENOMEM;
   s->L = L;
@@ -568,6 +590,7 @@ stage_status stage_init(int L, int hidden, int heads, int ffn, uint64_t seed, st
       stage_status st = dev_alloc(s, s->allocs, &s->param[l][w], n * param_esz(s, w));
       if (!st) st = dev_alloc(s, s->allocs, (void**)&s->grad[l][w], n * 4);
       if (st) {
+        g_init_err = s->err;
         for (void* p : s->allocs) (void)hipFree(p);
         delete s;
         return st;
@@ -593,6 +616,7 @@ stage_status stage_init(int L, int hidden, int heads, int ffn, uint64_t seed, st
   hipError_t e = hipGetLastError();
   if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
   if (e != hipSuccess) {
+    g_init_err = std::string("initialisation kernels: ") + hipGetErrorString(e);
     for (void* p : s->allocs) (void)hipFree(p);
     delete s;
     return STAGE_EHIP;
@@ -779,7 +803,7 @@ const char* stage_site_name(int site) {
   return (site >= 0 && site < SITE_COUNT) ? SITE_NAMES[site] : "";
 }
 
-const char* stage_last_error(const stage_t* s) { return s ? s->err.c_str() : "null handle"; }
+const char* stage_last_error(const stage_t* s) { return s ? s->err.c_str() : g_init_err.c_str(); }
 
 void stage_destroy(stage_t* s) {
   if (!s) return;
