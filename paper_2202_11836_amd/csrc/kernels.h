@@ -97,3 +97,34 @@ hipError_t softmax_fwd(const float* scores, const uint8_t* mask, T* P, int BH, i
 template <typename T>
 hipError_t softmax_bwd(const float* dP, const T* P, T* dS, int BH, int S, int ld, float scale,
                        hipStream_t st);
+
+// ---------------------------------------------------------------------------
+// Fused attention (bf16 stages, head dim 64).
+//   qkv:  [B*S, 3h] (Q | K | V, head j = columns 64 j .. 64 j + 63 of each)
+//   mask: [B, S] uint8 key mask; kext: [B] ints, 1 + last valid key
+//   out:  forward: context [B*S, h]; backward: dQKV [B*S, 3h]
+//   lse:  [B*H, S] fp32 log2-sum-exp of the scaled scores (forward output)
+//   o, dout: forward context and its gradient [B*S, h] (backward inputs)
+//   dsum: [B*H, S] fp32 rowsum(dO * O) (written by attn_backward_dq)
+// ---------------------------------------------------------------------------
+struct AttnArgs {
+  const bf16_t* qkv;
+  const uint8_t* mask;
+  const int* kext;
+  bf16_t* out;
+  float* lse;
+  const bf16_t* o;
+  const bf16_t* dout;
+  float* dsum;
+  int B, S, H, h;
+  float scale_log2;  // softmax scale * log2(e)
+  float scale;       // softmax scale
+};
+// kext[b] = 1 + last s with mask[b][s] != 0 (0 if none).
+hipError_t key_extent(const uint8_t* mask, int B, int S, int* kext, hipStream_t st);
+// Forward pass (needs kext).
+hipError_t attn_forward(const AttnArgs& a, hipStream_t st);
+// dsum and dQ (into out's Q block); must run before attn_backward_dkdv.
+hipError_t attn_backward_dq(const AttnArgs& a, hipStream_t st);
+// dK and dV (into out's K and V blocks).
+hipError_t attn_backward_dkdv(const AttnArgs& a, hipStream_t st);

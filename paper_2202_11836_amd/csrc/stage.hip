@@ -37,7 +37,9 @@ constexpr int COL_PARTS = 128; // row blocks of the bias-gradient column sums
   X(DP_BWD, "dp_gemm_bwd") X(SOFTMAX_BWD, "softmax_bwd") X(DV_BWD, "dv_gemm_bwd")        \
   X(DQ_BWD, "dq_gemm_bwd") X(DK_BWD, "dk_gemm_bwd") X(BQKV_SUM, "bqkv_colsum")           \
   X(BQKV_RED, "bqkv_colreduce") X(WQKV_WGRAD, "wqkv_wgrad_gemm")                        \
-  X(WQKV_RED, "wqkv_wgrad_splitk_reduce") X(QKV_DGRAD, "qkv_dgrad_resid_gemm")
+  X(WQKV_RED, "wqkv_wgrad_splitk_reduce") X(QKV_DGRAD, "qkv_dgrad_resid_gemm")            \
+  X(KEXT, "key_extent") X(ATTN_FWD, "attn_fwd") X(ATTN_DQ, "attn_bwd_dq")                 \
+  X(ATTN_DKDV, "attn_bwd_dkdv")
 
 enum Site {
 #define SITE_ENUM(id, name) SITE_##id,
@@ -92,7 +94,8 @@ bool is_matrix(int which) {
 struct Saved {
   void* X = nullptr;     // layer input [T, h]
   void* QKV = nullptr;   // [T, 3h]
-  void* P = nullptr;     // softmax probabilities [B*H, S, S]
+  void* P = nullptr;     // softmax probabilities [B*H, S, S] (fp32 stages)
+  float* lse = nullptr;  // log2-sum-exp of the scaled scores [B*H, S] (bf16 stages)
   void* C = nullptr;     // context [T, h]
   void* xhat1 = nullptr; // [T, h]
   float* rstd1 = nullptr;
@@ -115,13 +118,15 @@ struct stage {
   std::vector<void*> allocs;  // parameter / gradient memory
 
   // Activation memory, sized for cap_T tokens and cap_BSS score entries.
-  int64_t cap_T = -1, cap_BSS = -1;
+  int64_t cap_T = -1, cap_BSS = -1, cap_B = -1;
   std::vector<void*> act_allocs;
   std::vector<Saved> saved;
   uint8_t* mask = nullptr;
   float* tmp = nullptr;     // [T, h] fp32 GEMM output before LayerNorm
   float* h1f = nullptr;     // [T, h] fp32 copy of H1 (bf16 stages)
-  float* scores = nullptr;  // [B*H, S, S] fp32 (scores, then dP)
+  float* scores = nullptr;  // [B*H, S, S] fp32 (scores, then dP; fp32 stages)
+  int* kext = nullptr;      // [B] key extent of each sequence
+  float* dsum = nullptr;    // [B*H, S] rowsum(dO * O) (bf16 stages)
   void* dS = nullptr;       // [B*H, S, S]
   void* dQKV = nullptr;     // [T, 3h]
   void* dZ2 = nullptr;      // [T, h]
@@ -214,7 +219,7 @@ void free_activations(stage_t* s) {
   for (void* p : s->act_allocs) (void)hipFree(p);
   s->act_allocs.clear();
   s->saved.clear();
-  s->cap_T = s->cap_BSS = -1;
+  s->cap_T = s->cap_BSS = s->cap_B = -1;
   s->have_ctx = false;
 }
 
@@ -243,8 +248,11 @@ int choose_ksplit(int64_t tiles, int K) {
 
 stage_status ensure_activations(stage_t* s, int B, int S) {
   const int64_t T = (int64_t)B * S;
-  const int64_t BSS = (int64_t)B * s->H * S * S;
-  if (T <= s->cap_T && BSS <= s->cap_BSS && (int)s->saved.size() == s->L) return STAGE_OK;
+  // The score matrix is materialised only on fp32 stages.
+  const int64_t BSS = s->dtype == STAGE_F32 ? (int64_t)B * s->H * S * S : 0;
+  const int64_t BHS = (int64_t)B * s->H * S;
+  if (T <= s->cap_T && BSS <= s->cap_BSS && B <= s->cap_B && (int)s->saved.size() == s->L)
+    return STAGE_OK;
   free_activations(s);
   const size_t e = s->esz;
   const int64_t h = s->h, f = s->f;
@@ -254,7 +262,7 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
   for (int l = 0; l < s->L; ++l) {
     Saved& v = s->saved[l];
     if ((st = A(&v.X, T * h * e)) || (st = A(&v.QKV, T * 3 * h * e)) ||
-        (st = A(&v.P, BSS * e)) || (st = A(&v.C, T * h * e)) || (st = A(&v.xhat1, T * h * e)) ||
+        (st = A(&v.P, BSS * e)) || (st = A((void**)&v.lse, BHS * 4)) || (st = A(&v.C, T * h * e)) || (st = A(&v.xhat1, T * h * e)) ||
         (st = A((void**)&v.rstd1, T * 4)) || (st = A(&v.H1, T * h * e)) ||
         (st = A(&v.U, T * f * e)) || (st = A(&v.G, T * f * e)) ||
         (st = A(&v.xhat2, T * h * e)) || (st = A((void**)&v.rstd2, T * 4)))
@@ -263,6 +271,7 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
   if ((st = A((void**)&s->mask, T)) || (st = A((void**)&s->tmp, T * h * 4)) ||
       (st = A((void**)&s->h1f, T * h * 4)) ||
       (st = A((void**)&s->scores, BSS * 4)) || (st = A(&s->dS, BSS * e)) ||
+      (st = A((void**)&s->kext, (size_t)B * 4)) || (st = A((void**)&s->dsum, BHS * 4)) ||
       (st = A(&s->dQKV, T * 3 * h * e)) || (st = A(&s->dZ2, T * h * e)) ||
       (st = A(&s->dU, T * f * e)) || (st = A(&s->dH1, T * h * e)) ||
       (st = A(&s->dZ1, T * h * e)) || (st = A(&s->dC, T * h * e)) || (st = A(&s->dY, T * h * e)))
@@ -283,6 +292,7 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
   if ((st = A((void**)&s->splitk, std::max<size_t>(need, 1) * 4))) return st;
   s->cap_T = T;
   s->cap_BSS = BSS;
+  s->cap_B = B;
   return STAGE_OK;
 }
 
@@ -326,6 +336,23 @@ stage_status wgrad(stage_t* s, int site, int site_red, const T* dYm, int64_t ld_
   return STAGE_OK;
 }
 
+AttnArgs attn_args(stage_t* s, const bf16_t* qkv, bf16_t* out, float* lse) {
+  AttnArgs a{};
+  a.qkv = qkv;
+  a.mask = s->mask;
+  a.kext = s->kext;
+  a.out = out;
+  a.lse = lse;
+  a.dsum = s->dsum;
+  a.B = s->B;
+  a.S = s->S;
+  a.H = s->H;
+  a.h = s->h;
+  a.scale = 1.0f / sqrtf((float)HEAD_DIM);
+  a.scale_log2 = a.scale * 1.4426950408889634f;
+  return a;
+}
+
 template <typename T>
 stage_status forward_impl(stage_t* s, const T* x, T* y) {
   const int B = s->B, S = s->S, h = s->h, H = s->H, f = s->f;
@@ -334,6 +361,7 @@ stage_status forward_impl(stage_t* s, const T* x, T* y) {
   hipStream_t st = s->stream;
   const float scale = 1.0f / sqrtf((float)HEAD_DIM);
   HIPCK(hipMemcpyAsync(s->saved[0].X, x, (size_t)Tn * h * sizeof(T), hipMemcpyDeviceToDevice, st));
+  if (std::is_same<T, bf16_t>::value) SITE(KEXT, key_extent(s->mask, B, S, s->kext, st));
   for (int l = 0; l < s->L; ++l) {
     Saved& v = s->saved[l];
     auto& p = s->param[l];
@@ -345,6 +373,11 @@ stage_status forward_impl(stage_t* s, const T* x, T* y) {
       g.bias = (const float*)p[STAGE_B_QKV];
       SITE(QKV_FWD, Gemm<T>::run(g, true, true, EPI_STORE, false, 1, st));
     }
+    if constexpr (std::is_same<T, bf16_t>::value) {
+      // Fused attention: softmax(Q K^T / 8) V per (batch, head), P stays on chip.
+      AttnArgs aa = attn_args(s, (const bf16_t*)QKV, (bf16_t*)v.C, v.lse);
+      SITE(ATTN_FWD, attn_forward(aa, st));
+    } else {
     // scores[b, j] = Q_bj K_bj^T  (fp32)
     {
       GemmArgs g = gemm_args(QKV, 3 * h, QKV + h, 3 * h, s->scores, S, S, S, HEAD_DIM);
@@ -367,6 +400,7 @@ stage_status forward_impl(stage_t* s, const T* x, T* y) {
       g.sC1 = (int64_t)S * h;
       g.sC2 = HEAD_DIM;
       SITE(CTX_FWD, Gemm<T>::run(g, true, false, EPI_STORE, false, BH, st));
+    }
     }
     // tmp = C W_o^T (fp32);  H1 = LN(X + tmp + b_o)
     {
@@ -478,6 +512,13 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
       GemmArgs g = gemm_args(dZ1, h, p[STAGE_W_O], h, dC, h, Tn, h, h);
       SITE(OUT_DGRAD, Gemm<T>::run(g, true, false, EPI_STORE, false, 1, st));
     }
+    if constexpr (std::is_same<T, bf16_t>::value) {
+      AttnArgs aa = attn_args(s, (const bf16_t*)QKV, (bf16_t*)dQKV, v.lse);
+      aa.o = (const bf16_t*)v.C;
+      aa.dout = (const bf16_t*)dC;
+      SITE(ATTN_DQ, attn_backward_dq(aa, st));
+      SITE(ATTN_DKDV, attn_backward_dkdv(aa, st));
+    } else {
     // dP[b, j] = dC_bj V_bj^T (fp32, into the score buffer)
     {
       GemmArgs g = gemm_args(dC, h, QKV + 2 * h, 3 * h, s->scores, S, S, S, HEAD_DIM);
@@ -527,6 +568,7 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
       g.sC1 = (int64_t)S * 3 * h;
       g.sC2 = HEAD_DIM;
       SITE(DK_BWD, Gemm<T>::run(g, false, false, EPI_STORE, false, BH, st));
+    }
     }
     if ((r = col_sum<T>(s, SITE_BQKV_SUM, SITE_BQKV_RED, dQKV, 3 * h, gr[STAGE_B_QKV]))) return r;
     // dW_qkv = dQKV^T X
@@ -641,9 +683,7 @@ stage_status stage_forward(stage_t* s, const void* x, const uint8_t* key_mask, i
   if (T > 0 && x == y) return fail(s, STAGE_EINVAL, "x and y may not alias");
   if (T * std::max(3 * s->h, s->f) >= (int64_t)1 << 31)
     return fail(s, STAGE_EINVAL, "batch * seq too large");
-  if (s->dtype == STAGE_BF16 && seq % 8 != 0)
-    return fail(s, STAGE_EINVAL, "bf16 stages need seq to be a multiple of 8");
-  if ((int64_t)batch * s->H * seq * seq >= (int64_t)1 << 40)
+  if (s->dtype == STAGE_F32 && (int64_t)batch * s->H * seq * seq >= (int64_t)1 << 40)
     return fail(s, STAGE_EINVAL, "score matrix too large");
   stage_status st = ensure_activations(s, batch, seq);
   if (st) return st;

@@ -38,8 +38,12 @@ def test_forward_backward_state_errors():
     with pytest.raises(StageError) as e:  # context consumed
         st.backward(dy)
     assert e.value.status == 2
-    with pytest.raises(StageError) as e:  # bf16 seq must be a multiple of 8
-        st.forward(torch.zeros(2, 13, 128, dtype=torch.bfloat16, device="cuda"))
+    from paper_2202_11836_amd import stage_forward
+    with pytest.raises(StageError) as e:  # null y
+        stage_forward(st.handle, x, None, 2, 16, None)
+    assert e.value.status == 1
+    with pytest.raises(StageError) as e:  # x and y alias
+        stage_forward(st.handle, x, None, 2, 16, x)
     assert e.value.status == 1
     with pytest.raises(StageError):
         st.param(1, 0)
