@@ -46,12 +46,33 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
-// Exact GELU u * Phi(u) and its derivative Phi(u) + u * phi(u), using the
-// device math library's erff / expf.
+// GELU u * Phi(u) = u/2 * (1 + erf(u / sqrt 2)) and its derivative
+// Phi(u) + u * phi(u).  erf is evaluated with the rational approximation of
+// Abramowitz & Stegun, Handbook of Mathematical Functions, formula 7.1.26
+// (after Hastings): erf(x) = 1 - (a1 t + ... + a5 t^5) exp(-x^2),
+// t = 1 / (1 + p x), x >= 0, |error| <= 1.5e-7.  It is branch-free, and the
+// exp(-x^2) = exp(-u^2 / 2) term is shared with the derivative.
+struct ErfParts {
+  float onep;  // 1 + erf(u / sqrt 2) = 2 Phi(u), without cancellation for u < 0
+  float e;     // exp(-u^2 / 2)
+};
+__device__ __forceinline__ ErfParts erf_parts(float u) {
+  const float x = u * 0.70710678118654752f;
+  const float ax = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, ax, 1.0f));
+  const float poly =
+      t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, 1.061405429f, -1.453152027f), 1.421413741f),
+                       -0.284496736f),
+               0.254829592f);
+  const float e = __builtin_amdgcn_exp2f(-x * x * 1.4426950408889634f);
+  const float erfc_ax = poly * e;  // 1 - erf(|x|)
+  return {x < 0.0f ? erfc_ax : 2.0f - erfc_ax, e};
+}
 __device__ __forceinline__ float gelu_f(float u) {
-  return 0.5f * u * (1.0f + erff(u * 0.70710678118654752f));
+  const ErfParts p = erf_parts(u);
+  return 0.5f * u * p.onep;
 }
 __device__ __forceinline__ float gelu_grad_f(float u) {
-  return 0.5f * (1.0f + erff(u * 0.70710678118654752f)) +
-         u * expf(-0.5f * u * u) * 0.39894228040143268f;
+  const ErfParts p = erf_parts(u);
+  return fmaf(u * 0.39894228040143268f, p.e, 0.5f * p.onep);
 }

@@ -43,44 +43,187 @@ __device__ __forceinline__ int64_t batch_off(int zb, int zdiv, int64_t s1, int64
   return (int64_t)(zb / zdiv) * s1 + (int64_t)(zb % zdiv) * s2;
 }
 
-template <int EPI, bool OUTF32>
-__device__ __forceinline__ void epi_store(const GemmArgs& g, int64_t offC, int64_t offAux, int zs,
-                                          int m, int n, float v) {
-  if (EPI == EPI_PARTIAL) {
-    float* C = (float*)g.C + (int64_t)zs * g.M * g.ldc;
-    C[(int64_t)m * g.ldc + n] = v;
-  } else if (EPI == EPI_STORE) {
-    v *= g.alpha;
-    if (g.bias) v += g.bias[n];
-    if (OUTF32)
-      ((float*)g.C + offC)[(int64_t)m * g.ldc + n] = v;
-    else
-      ((bf16_t*)g.C + offC)[(int64_t)m * g.ldc + n] = f2bf(v);
-  } else if (EPI == EPI_GELU) {
-    float u = v + g.bias[n];
-    bf16_t ub = f2bf(u);
-    ((bf16_t*)g.C + offC)[(int64_t)m * g.ldc + n] = ub;
-    // GELU of the stored (rounded) U so that forward and backward agree.
-    ((bf16_t*)g.C2 + offC)[(int64_t)m * g.ldc + n] = f2bf(gelu_f(bf2f(ub)));
-  } else if (EPI == EPI_DGELU) {
-    float u = bf2f(((const bf16_t*)g.aux + offAux)[(int64_t)m * g.ldaux + n]);
-    ((bf16_t*)g.C + offC)[(int64_t)m * g.ldc + n] = f2bf(v * gelu_grad_f(u));
-  } else if (EPI == EPI_RESID) {
-    float r = bf2f(((const bf16_t*)g.aux + offAux)[(int64_t)m * g.ldaux + n]);
-    ((bf16_t*)g.C + offC)[(int64_t)m * g.ldc + n] = f2bf(v + r);
+// ---------------------------------------------------------------------------
+// bf16 MFMA GEMM
+//
+// Block = 4 wavefronts in a 2 x 2 grid over a BM x BN tile; each wavefront
+// owns (BM/2) x (BN/2) = TM x TN accumulators of 32 x 32.  k-tiles of 64 are
+// double-buffered in LDS (up to 147 KB of gfx950's 160 KB per CU): the next tile is fetched into registers while the
+// current one feeds the MFMAs, then written to the other LDS buffer, so one
+// barrier per k-tile suffices.  The epilogue stages each 32-row slab of a
+// wavefront's accumulators through LDS (fp32) so that bias / activation /
+// residual operands are read and the results written as 16-byte row
+// segments.
+// ---------------------------------------------------------------------------
+template <int BM, int BN>
+struct TileCfg {
+  static constexpr int BK = 64;
+  static constexpr int LDS_LD = BK + 8;  // 144-byte rows: fragment reads of 8 rows hit distinct banks
+  static constexpr int WM = BM / 2, WN = BN / 2;
+  static constexpr int TM = WM / 32, TN = WN / 32;
+  static constexpr int BUF = (BM + BN) * LDS_LD;  // elements per buffer
+  static constexpr int EPI_LD = WN + 4;          // fp32 staging row
+  static constexpr int LDS_BYTES_MAIN = 2 * BUF * 2;
+  static constexpr int LDS_BYTES_EPI = 4 * 32 * EPI_LD * 4;
+  static constexpr int LDS_BYTES = LDS_BYTES_MAIN > LDS_BYTES_EPI ? LDS_BYTES_MAIN : LDS_BYTES_EPI;
+};
+
+// Buffer resource over [base, base + bytes): loads past the end return 0.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  const int nrec = (int)(bytes < 0 ? 0 : (bytes > 0x7fffffff ? 0x7fffffff : bytes));
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, nrec, 0x00020000);
+}
+
+__device__ __forceinline__ u32x4_t buf_load16(__amdgpu_buffer_rsrc_t r, int byte_off) {
+  return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0));
+}
+
+// Global -> registers for one operand tile of k-tile k0 (relative to the
+// resource's first k).  k-major: the resource starts at the tile's first
+// row and ends at the operand's last valid row, so rows past it read 0 (K is
+// a multiple of BK for k-major operands).  m/n-major: the resource spans this
+// split's k rows [kbeg, K), so k rows past K read 0; columns past lim are
+// zeroed by a select.
+template <int R, int BK, bool KMAJ>
+__device__ __forceinline__ void g2r(__amdgpu_buffer_rsrc_t rs, int64_t ld, int r0, int lim, int k0,
+                                    u32x4_t* regs) {
+  const int tid = threadIdx.x;
+  if constexpr (KMAJ) {
+    constexpr int VPR = BK / 8;
+#pragma unroll
+    for (int i = 0; i < R * VPR / NT; ++i) {
+      const int v = tid + NT * i;
+      const int row = v / VPR, kc = (v % VPR) * 8;
+      regs[i] = buf_load16(rs, (int)(((int64_t)row * ld + k0 + kc) * 2));
+    }
+  } else {
+    constexpr int KBN = BK / 4, NBLK = R * BK / 32;
+#pragma unroll
+    for (int i = 0; i < (NBLK + NT - 1) / NT; ++i) {
+      const int blk = tid + NT * i;
+      const int kb = blk % KBN, cb = blk / KBN;
+      const int gc = r0 + cb * 8;
+      const bool ok = blk < NBLK && gc < lim;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int gk = k0 + kb * 4 + j;
+        const u32x4_t v = buf_load16(rs, (int)(((int64_t)gk * ld + (ok ? gc : 0)) * 2));
+        regs[4 * i + j] = ok ? v : u32x4_t{0, 0, 0, 0};
+      }
+    }
   }
 }
 
-// ---------------------------------------------------------------------------
-// bf16 MFMA GEMM
-// ---------------------------------------------------------------------------
-template <int BM, int BN, int BK, bool AK, bool BKM, int EPI, bool OUTF32>
-__global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
-  constexpr int LDS_LD = BK + 8;  // padded row (elements)
-  constexpr int TM = BM / 64;     // 32x32 MFMA tiles per wavefront along m
-  constexpr int TN = BN / 64;
-  __shared__ __attribute__((aligned(16))) bf16_t As[BM * LDS_LD];
-  __shared__ __attribute__((aligned(16))) bf16_t Bs[BN * LDS_LD];
+// Registers -> LDS tile S[R][LDS_LD] (k contiguous).  An m/n-major operand is
+// transposed in registers: 4 k-rows x 8 columns become 8 rows of 4 k.
+template <int R, int BK, int LDS_LD, bool KMAJ>
+__device__ __forceinline__ void r2s(bf16_t* S, const u32x4_t* regs) {
+  const int tid = threadIdx.x;
+  if constexpr (KMAJ) {
+    constexpr int VPR = BK / 8;
+#pragma unroll
+    for (int i = 0; i < R * VPR / NT; ++i) {
+      const int v = tid + NT * i;
+      const int row = v / VPR, kc = (v % VPR) * 8;
+      *(u32x4_t*)(S + row * LDS_LD + kc) = regs[i];
+    }
+  } else {
+    constexpr int KBN = BK / 4, NBLK = R * BK / 32;
+#pragma unroll
+    for (int i = 0; i < (NBLK + NT - 1) / NT; ++i) {
+      const int blk = tid + NT * i;
+      if (blk >= NBLK) continue;
+      const int kb = blk % KBN, cb = blk / KBN;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const int w = c >> 1, sh = (c & 1) * 16;
+        const uint32_t e0 = (regs[4 * i + 0][w] >> sh) & 0xffffu;
+        const uint32_t e1 = (regs[4 * i + 1][w] >> sh) & 0xffffu;
+        const uint32_t e2 = (regs[4 * i + 2][w] >> sh) & 0xffffu;
+        const uint32_t e3 = (regs[4 * i + 3][w] >> sh) & 0xffffu;
+        *(u32x2_t*)(S + (cb * 8 + c) * LDS_LD + kb * 4) = u32x2_t{e0 | (e1 << 16), e2 | (e3 << 16)};
+      }
+    }
+  }
+}
+
+template <int R, int BK, bool KMAJ>
+constexpr int stage_regs() {
+  return KMAJ ? R * (BK / 8) / NT : 4 * ((R * BK / 32 + NT - 1) / NT);
+}
+
+__device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)a) |
+         ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)b) << 16);
+}
+
+// Epilogue for 8 consecutive columns n..n+7 of row m (n % 8 == 0, n < N).
+template <int EPI, bool OUTF32>
+__device__ __forceinline__ void epi8(const GemmArgs& g, int64_t offC, int zs, int m, int n,
+                                     float v[8]) {
+  const int64_t idx = (int64_t)m * g.ldc + n;
+  if (EPI == EPI_PARTIAL) {
+    float* C = (float*)g.C + (int64_t)zs * g.M * g.ldc + idx;
+    *(f32x4_t*)C = f32x4_t{v[0], v[1], v[2], v[3]};
+    *(f32x4_t*)(C + 4) = f32x4_t{v[4], v[5], v[6], v[7]};
+    return;
+  }
+  if (EPI == EPI_STORE || EPI == EPI_GELU) {
+    if (EPI == EPI_STORE) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] *= g.alpha;
+    }
+    if (g.bias) {
+      const f32x4_t b0 = *(const f32x4_t*)(g.bias + n), b1 = *(const f32x4_t*)(g.bias + n + 4);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        v[i] += b0[i];
+        v[4 + i] += b1[i];
+      }
+    }
+  }
+  if (EPI == EPI_STORE && OUTF32) {
+    float* C = (float*)g.C + offC + idx;
+    *(f32x4_t*)C = f32x4_t{v[0], v[1], v[2], v[3]};
+    *(f32x4_t*)(C + 4) = f32x4_t{v[4], v[5], v[6], v[7]};
+    return;
+  }
+  if (EPI == EPI_DGELU || EPI == EPI_RESID) {
+    const u32x4_t x = *(const u32x4_t*)((const bf16_t*)g.aux + offC + (int64_t)m * g.ldaux + n);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float a0 = __uint_as_float(x[i] << 16), a1 = __uint_as_float(x[i] & 0xffff0000u);
+      if (EPI == EPI_DGELU) {
+        v[2 * i] *= gelu_grad_f(a0);
+        v[2 * i + 1] *= gelu_grad_f(a1);
+      } else {
+        v[2 * i] += a0;
+        v[2 * i + 1] += a1;
+      }
+    }
+  }
+  u32x4_t o;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) o[i] = pack_bf2(v[2 * i], v[2 * i + 1]);
+  *(u32x4_t*)((bf16_t*)g.C + offC + idx) = o;
+  if (EPI == EPI_GELU) {
+    // GELU of the stored (rounded) U, so that forward and backward agree.
+    u32x4_t q;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float u0 = __uint_as_float(o[i] << 16), u1 = __uint_as_float(o[i] & 0xffff0000u);
+      q[i] = pack_bf2(gelu_f(u0), gelu_f(u1));
+    }
+    *(u32x4_t*)((bf16_t*)g.C2 + offC + idx) = q;
+  }
+}
+
+template <int BM, int BN, bool AK, bool BKM, int EPI, bool OUTF32>
+__global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
+  using C = TileCfg<BM, BN>;
+  constexpr int BK = C::BK, LDS_LD = C::LDS_LD, TM = C::TM, TN = C::TN;
+  __shared__ __attribute__((aligned(16))) unsigned char smem_raw[C::LDS_BYTES];
+  bf16_t* smem = (bf16_t*)smem_raw;
 
   const int nbm = (g.M + BM - 1) / BM, nbn = (g.N + BN - 1) / BN;
   int tm, tn;
@@ -93,95 +236,31 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
   const int kbeg = zs * g.kchunk;
   const int kend = min(g.K, kbeg + g.kchunk);
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
+  const int hf = lane >> 5, rr = lane & 31;
 
-  // Staging registers: each thread moves 16-byte vectors.  A k-major operand
-  // tile is R rows of BK/8 vectors; an m/n-major one is (BK/4) x (R/8) blocks
-  // of 4 k-rows x 8 columns (4 vectors each).
-  constexpr int A_KV = BM * BK / 8 / NT, B_KV = BN * BK / 8 / NT;
-  constexpr int A_BLK = (BM * BK / 32 + NT - 1) / NT, B_BLK = (BN * BK / 32 + NT - 1) / NT;
-  constexpr int A_REGS = AK ? A_KV : 4 * A_BLK;
-  constexpr int B_REGS = BKM ? B_KV : 4 * B_BLK;
-  static_assert(A_KV >= 1 && B_KV >= 1, "tile too small");
-  u32x4_t ra[A_REGS], rb[B_REGS];
+  constexpr int AR = stage_regs<BM, BK, AK>(), BR = stage_regs<BN, BK, BKM>();
+  u32x4_t ra[AR], rb[BR];
 
-  // Global -> registers for one operand (R rows/columns starting at r0, lim
-  // valid), k range [k0, k0 + BK) clipped to kend; out of range reads 0.
-  auto load_tile = [&](const bf16_t* __restrict__ X, int64_t ld, auto kmaj_tag, auto R_tag,
-                       int r0, int lim, int k0, u32x4_t* regs) {
-    constexpr bool KMAJ = decltype(kmaj_tag)::value;
-    constexpr int R = decltype(R_tag)::value;
-    if constexpr (KMAJ) {
-      constexpr int VPR = BK / 8;
-#pragma unroll
-      for (int i = 0; i < R * BK / 8 / NT; ++i) {
-        int v = tid + NT * i;
-        int row = v / VPR, kc = (v % VPR) * 8;
-        int gr = r0 + row, gk = k0 + kc;
-        if (gr < lim && gk < kend)
-          regs[i] = *(const u32x4_t*)(X + (int64_t)gr * ld + gk);
-        else
-          regs[i] = u32x4_t{0, 0, 0, 0};
-      }
-    } else {
-      constexpr int KBN = BK / 4, NBLK = R * BK / 32;
-#pragma unroll
-      for (int i = 0; i < (NBLK + NT - 1) / NT; ++i) {
-        int blk = tid + NT * i;
-        int kb = blk % KBN, cb = blk / KBN;
-        int gc = r0 + cb * 8;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          int gk = k0 + kb * 4 + j;
-          if (blk < NBLK && gc < lim && gk < kend)
-            regs[4 * i + j] = *(const u32x4_t*)(X + (int64_t)gk * ld + gc);
-          else
-            regs[4 * i + j] = u32x4_t{0, 0, 0, 0};
-        }
-      }
-    }
-  };
-
-  auto store_tile = [&](bf16_t* S, auto kmaj_tag, auto R_tag, const u32x4_t* regs) {
-    constexpr bool KMAJ = decltype(kmaj_tag)::value;
-    constexpr int R = decltype(R_tag)::value;
-    if constexpr (KMAJ) {
-      constexpr int VPR = BK / 8;
-#pragma unroll
-      for (int i = 0; i < R * BK / 8 / NT; ++i) {
-        int v = tid + NT * i;
-        int row = v / VPR, kc = (v % VPR) * 8;
-        *(u32x4_t*)(S + row * LDS_LD + kc) = regs[i];
-      }
-    } else {
-      constexpr int KBN = BK / 4, NBLK = R * BK / 32;
-#pragma unroll
-      for (int i = 0; i < (NBLK + NT - 1) / NT; ++i) {
-        int blk = tid + NT * i;
-        if (blk >= NBLK) continue;
-        int kb = blk % KBN, cb = blk / KBN;
-        // regs[4i + j] holds columns cb*8 .. cb*8+7 of k-row kb*4 + j;
-        // write column c as the 4 consecutive k values of that column.
-#pragma unroll
-        for (int c = 0; c < 8; ++c) {
-          const int w = c >> 1, sh = (c & 1) * 16;
-          uint32_t e0 = (regs[4 * i + 0][w] >> sh) & 0xffffu;
-          uint32_t e1 = (regs[4 * i + 1][w] >> sh) & 0xffffu;
-          uint32_t e2 = (regs[4 * i + 2][w] >> sh) & 0xffffu;
-          uint32_t e3 = (regs[4 * i + 3][w] >> sh) & 0xffffu;
-          u32x2_t o = {e0 | (e1 << 16), e2 | (e3 << 16)};
-          *(u32x2_t*)(S + (cb * 8 + c) * LDS_LD + kb * 4) = o;
-        }
-      }
-    }
-  };
-  using AKT = std::integral_constant<bool, AK>;
-  using BKT = std::integral_constant<bool, BKM>;
-  using BMT = std::integral_constant<int, BM>;
-  using BNT = std::integral_constant<int, BN>;
+  // Buffer resources (see g2r); k offsets passed to g2r are relative to kbeg
+  // for m/n-major operands and absolute for k-major ones.
+  __amdgpu_buffer_rsrc_t rsA, rsB;
+  int kA0, kB0;
+  if constexpr (AK) {
+    rsA = make_rsrc(A + (int64_t)m0 * g.lda, (int64_t)(g.M - m0) * g.lda * 2);
+    kA0 = kbeg;
+  } else {
+    rsA = make_rsrc(A + (int64_t)kbeg * g.lda, (int64_t)(g.K - kbeg) * g.lda * 2);
+    kA0 = 0;
+  }
+  if constexpr (BKM) {
+    rsB = make_rsrc(B + (int64_t)n0 * g.ldb, (int64_t)(g.N - n0) * g.ldb * 2);
+    kB0 = kbeg;
+  } else {
+    rsB = make_rsrc(B + (int64_t)kbeg * g.ldb, (int64_t)(g.K - kbeg) * g.ldb * 2);
+    kB0 = 0;
+  }
 
   f32x16_t acc[TM][TN];
 #pragma unroll
@@ -193,63 +272,92 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
 
   const int ntiles = (kend - kbeg + BK - 1) / BK;
   if (ntiles > 0) {
-    load_tile(A, g.lda, AKT{}, BMT{}, m0, g.M, kbeg, ra);
-    load_tile(B, g.ldb, BKT{}, BNT{}, n0, g.N, kbeg, rb);
-    store_tile(As, AKT{}, BMT{}, ra);
-    store_tile(Bs, BKT{}, BNT{}, rb);
+    g2r<BM, BK, AK>(rsA, g.lda, m0, g.M, kA0, ra);
+    g2r<BN, BK, BKM>(rsB, g.ldb, n0, g.N, kB0, rb);
+    r2s<BM, BK, LDS_LD, AK>(smem, ra);
+    r2s<BN, BK, LDS_LD, BKM>(smem + BM * LDS_LD, rb);
     __syncthreads();
   }
+  constexpr int KS = BK / 16;
   for (int t = 0; t < ntiles; ++t) {
+    const bf16_t* As = smem + (t & 1) * C::BUF;
+    const bf16_t* Bs = As + BM * LDS_LD;
     const bool more = t + 1 < ntiles;
     if (more) {
-      int k0 = kbeg + (t + 1) * BK;
-      load_tile(A, g.lda, AKT{}, BMT{}, m0, g.M, k0, ra);
-      load_tile(B, g.ldb, BKT{}, BNT{}, n0, g.N, k0, rb);
+      g2r<BM, BK, AK>(rsA, g.lda, m0, g.M, kA0 + (t + 1) * BK, ra);
+      g2r<BN, BK, BKM>(rsB, g.ldb, n0, g.N, kB0 + (t + 1) * BK, rb);
     }
+    // Fragments of k-step ks + 1 are read while the MFMAs of ks run.
+    bf16x8_t af[2][TM], bfr[2][TN];
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8_t af[TM], bfr[TN];
-      const int kofs = ks * 16 + (lane >> 5) * 8;
+    for (int i = 0; i < TM; ++i)
+      af[0][i] = *(const bf16x8_t*)(As + (wm * C::WM + i * 32 + rr) * LDS_LD + hf * 8);
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        int row = wm * (BM / 2) + i * 32 + (lane & 31);
-        af[i] = *(const bf16x8_t*)(As + row * LDS_LD + kofs);
+    for (int j = 0; j < TN; ++j)
+      bfr[0][j] = *(const bf16x8_t*)(Bs + (wn * C::WN + j * 32 + rr) * LDS_LD + hf * 8);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int cur = ks & 1, nxt = cur ^ 1;
+      if (ks + 1 < KS) {
+        const int kofs = (ks + 1) * 16 + hf * 8;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          af[nxt][i] = *(const bf16x8_t*)(As + (wm * C::WM + i * 32 + rr) * LDS_LD + kofs);
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          bfr[nxt][j] = *(const bf16x8_t*)(Bs + (wn * C::WN + j * 32 + rr) * LDS_LD + kofs);
       }
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        int row = wn * (BN / 2) + j * 32 + (lane & 31);
-        bfr[j] = *(const bf16x8_t*)(Bs + row * LDS_LD + kofs);
+      if (ks == KS - 1 && more) {
+        // The next tile goes to the other buffer while the last MFMAs run.
+        bf16_t* An = smem + ((t + 1) & 1) * C::BUF;
+        r2s<BM, BK, LDS_LD, AK>(An, ra);
+        r2s<BN, BK, LDS_LD, BKM>(An + BM * LDS_LD, rb);
       }
+      // Keep the scheduler from sinking the fragment reads of ks + 1 down to
+      // their uses: they must be in flight while these MFMAs execute.
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          acc[i][j] =
+              __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
     __syncthreads();
-    if (more) {
-      store_tile(As, AKT{}, BMT{}, ra);
-      store_tile(Bs, BKT{}, BNT{}, rb);
-      __syncthreads();
-    }
   }
 
   // Epilogue.  32x32 accumulator layout: lane holds column (lane % 32);
   // register r holds row 8 * (r / 4) + 4 * (lane / 32) + (r % 4).
   const int64_t offC = batch_off(zb, g.zdiv, g.sC1, g.sC2);
-  const int64_t offAux = offC;  // aux shares C's batch layout
+  float* stg = (float*)smem_raw + wave * 32 * C::EPI_LD;
+  const int mw = m0 + wm * C::WM, nw = n0 + wn * C::WN;
+  constexpr int CH = C::WN / 8;  // 8-column chunks per staged row
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+  for (int i = 0; i < TM; ++i) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      int n = n0 + wn * (BN / 2) + j * 32 + (lane & 31);
-      if (n >= g.N) continue;
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        int m = m0 + wm * (BM / 2) + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (m < g.M) epi_store<EPI, OUTF32>(g, offC, offAux, zs, m, n, acc[i][j][r]);
+      for (int r = 0; r < 16; ++r)
+        stg[(8 * (r >> 2) + 4 * hf + (r & 3)) * C::EPI_LD + j * 32 + rr] = acc[i][j][r];
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int q = 0; q < 32 * CH / 64; ++q) {
+      const int c = lane + 64 * q;
+      const int row = c / CH, col = (c % CH) * 8;
+      const int m = mw + i * 32 + row, n = nw + col;
+      float v[8];
+      const f32x4_t x0 = *(const f32x4_t*)(stg + row * C::EPI_LD + col);
+      const f32x4_t x1 = *(const f32x4_t*)(stg + row * C::EPI_LD + col + 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[e] = x0[e];
+        v[4 + e] = x1[e];
       }
+      if (m < g.M && n < g.N) epi8<EPI, OUTF32>(g, offC, zs, m, n, v);
     }
+    __builtin_amdgcn_wave_barrier();
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -350,8 +458,7 @@ template <int BM, int BN, bool AK, bool BKM, int EPI, bool OUTF32>
 hipError_t launch_bf16(const GemmArgs& g, int batch, hipStream_t st) {
   int nbm = (g.M + BM - 1) / BM, nbn = (g.N + BN - 1) / BN;
   dim3 grid(nbm * nbn, 1, batch * g.ksplit);
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, 64, AK, BKM, EPI, OUTF32>), grid, dim3(NT), 0, st,
-                     g);
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, AK, BKM, EPI, OUTF32>), grid, dim3(NT), 0, st, g);
   return hipGetLastError();
 }
 
@@ -404,9 +511,18 @@ hipError_t dispatch_f32(const GemmArgs& g, GemmEpi epi, int batch, hipStream_t s
 hipError_t gemm_bf16(const GemmArgs& g, bool a_kmajor, bool b_kmajor, GemmEpi epi, bool out_f32,
                      int batch, hipStream_t st) {
   if (g.M <= 0 || g.N <= 0 || batch <= 0) return hipSuccess;
-  // Narrow outputs (one attention head, 64 columns) take a 128 x 64 tile.
-  if (g.N <= 64) return dispatch_layout<128, 64>(g, a_kmajor, b_kmajor, epi, out_f32, batch, st);
-  return dispatch_layout<128, 128>(g, a_kmajor, b_kmajor, epi, out_f32, batch, st);
+  // Vector epilogue and m/n-major staging work in 8-column units; k-tiles of
+  // 64 never straddle a split boundary, and k-major operands are read
+  // without a k bound.
+  if (g.N % 8 != 0 || g.ldc % 8 != 0) return hipErrorInvalidValue;
+  if (g.ksplit > 1 && g.kchunk % 64 != 0) return hipErrorInvalidValue;
+  if ((a_kmajor || b_kmajor) && g.K % 64 != 0) return hipErrorInvalidValue;
+  if ((!a_kmajor && g.M % 8 != 0) || (g.lda % 8 != 0) || (g.ldb % 8 != 0)) return hipErrorInvalidValue;
+  const int64_t t256 = (int64_t)((g.M + 255) / 256) * ((g.N + 255) / 256) * batch * g.ksplit;
+  if (t256 >= 512) return dispatch_layout<256, 256>(g, a_kmajor, b_kmajor, epi, out_f32, batch, st);
+  if (g.N <= 128 || t256 < 128)
+    return dispatch_layout<128, 128>(g, a_kmajor, b_kmajor, epi, out_f32, batch, st);
+  return dispatch_layout<256, 128>(g, a_kmajor, b_kmajor, epi, out_f32, batch, st);
 }
 
 hipError_t gemm_f32(const GemmArgs& g, bool a_kmajor, bool b_kmajor, GemmEpi epi, int batch,

@@ -79,6 +79,9 @@ template <typename T>
 hipError_t ln_bwd(const T* dy, const T* xhat, const float* rstd, const float* gamma, T* dz,
                   float* part, int rows, int h, hipStream_t st);
 
+// dst[c][r] = src[r][c] for a bf16 [R][C] matrix.
+hipError_t transpose_bf16(const bf16_t* src, int R, int C, bf16_t* dst, hipStream_t st);
+
 // part[blk][n] = sum over the block's rows of x[row][n].
 template <typename T>
 hipError_t col_partial(const T* x, int rows, int n, float* part, int nblk, hipStream_t st);

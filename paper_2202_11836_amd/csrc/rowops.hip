@@ -298,7 +298,31 @@ __global__ __launch_bounds__(256) void softmax_bwd_kernel(const float* __restric
   }
 }
 
+// dst[c][r] = src[r][c] for a bf16 [R][C] matrix; 64 x 64 tiles through LDS.
+__global__ __launch_bounds__(256) void transpose_bf16_kernel(const bf16_t* __restrict__ src, int R,
+                                                             int C, bf16_t* __restrict__ dst) {
+  __shared__ bf16_t t[64][66];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int r = r0 + i, c = c0 + tx;
+    t[i][tx] = (r < R && c < C) ? src[(int64_t)r * C + c] : (bf16_t)0;
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const int c = c0 + i, r = r0 + tx;
+    if (c < C && r < R) dst[(int64_t)c * R + r] = t[tx][i];
+  }
+}
+
 }  // namespace
+
+hipError_t transpose_bf16(const bf16_t* src, int R, int C, bf16_t* dst, hipStream_t st) {
+  if (R <= 0 || C <= 0) return hipSuccess;
+  hipLaunchKernelGGL(transpose_bf16_kernel, dim3((C + 63) / 64, (R + 63) / 64), dim3(256), 0, st,
+                     src, R, C, dst);
+  return hipGetLastError();
+}
 
 template <typename T, typename TA, typename TR>
 hipError_t add_ln_fwd(const TA* a, const float* bias, const TR* resid, const float* gamma,

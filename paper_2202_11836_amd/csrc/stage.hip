@@ -39,7 +39,7 @@ constexpr int COL_PARTS = 128; // row blocks of the bias-gradient column sums
   X(BQKV_RED, "bqkv_colreduce") X(WQKV_WGRAD, "wqkv_wgrad_gemm")                        \
   X(WQKV_RED, "wqkv_wgrad_splitk_reduce") X(QKV_DGRAD, "qkv_dgrad_resid_gemm")            \
   X(KEXT, "key_extent") X(ATTN_FWD, "attn_fwd") X(ATTN_DQ, "attn_bwd_dq")                 \
-  X(ATTN_DKDV, "attn_bwd_dkdv")
+  X(ATTN_DKDV, "attn_bwd_dkdv") X(WT, "weight_transpose")
 
 enum Site {
 #define SITE_ENUM(id, name) SITE_##id,
@@ -136,6 +136,12 @@ struct stage {
   void* dC = nullptr;       // [T, h]
   void* dY = nullptr;       // [T, h] gradient flowing between layers
   float* part = nullptr;    // column-sum partials
+  // Transposed weights of the layer being differentiated (bf16 stages), so
+  // that every data-gradient GEMM reads both operands k-contiguously.
+  void* wt_qkv = nullptr;   // [h, 3h]
+  void* wt_o = nullptr;     // [h, h]
+  void* wt_1 = nullptr;     // [h, f]
+  void* wt_2 = nullptr;     // [f, h]
   float* splitk = nullptr;  // split-K partials of the weight gradients
   size_t splitk_elems = 0;
 
@@ -275,6 +281,9 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
       (st = A(&s->dQKV, T * 3 * h * e)) || (st = A(&s->dZ2, T * h * e)) ||
       (st = A(&s->dU, T * f * e)) || (st = A(&s->dH1, T * h * e)) ||
       (st = A(&s->dZ1, T * h * e)) || (st = A(&s->dC, T * h * e)) || (st = A(&s->dY, T * h * e)))
+    return st;
+  if ((st = A(&s->wt_qkv, 3 * h * h * e)) || (st = A(&s->wt_o, h * h * e)) ||
+      (st = A(&s->wt_1, f * h * e)) || (st = A(&s->wt_2, h * f * e)))
     return st;
   const int64_t maxw = std::max<int64_t>(3 * h, f);
   const int64_t part_elems =
@@ -478,6 +487,23 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
     T* dC = (T*)s->dC;
     T* dQKV = (T*)s->dQKV;
     const T* QKV = (const T*)v.QKV;
+    // Data-gradient GEMMs multiply by W (not W^T); on bf16 stages W is first
+    // transposed so that both MFMA operands are k-contiguous.
+    constexpr bool kBF = std::is_same<T, bf16_t>::value;
+    const void* Wq = p[STAGE_W_QKV];
+    const void* Wo = p[STAGE_W_O];
+    const void* W1 = p[STAGE_W_1];
+    const void* W2 = p[STAGE_W_2];
+    if (kBF) {
+      SITE(WT, transpose_bf16((const bf16_t*)Wq, 3 * h, h, (bf16_t*)s->wt_qkv, st));
+      SITE(WT, transpose_bf16((const bf16_t*)Wo, h, h, (bf16_t*)s->wt_o, st));
+      SITE(WT, transpose_bf16((const bf16_t*)W1, f, h, (bf16_t*)s->wt_1, st));
+      SITE(WT, transpose_bf16((const bf16_t*)W2, h, f, (bf16_t*)s->wt_2, st));
+      Wq = s->wt_qkv;
+      Wo = s->wt_o;
+      W1 = s->wt_1;
+      W2 = s->wt_2;
+    }
     // Y = LN(Z2): dZ2, dgamma2, dbeta2, and db_2 = sum_t dZ2
     if ((r = ln_backward<T>(s, SITE_LN2_BWD, SITE_LN2_RED, dYcur, (const T*)v.xhat2, v.rstd2, (const float*)p[STAGE_G2], dZ2,
                             gr[STAGE_G2], gr[STAGE_BE2], gr[STAGE_B_2])))
@@ -486,20 +512,20 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
     if ((r = wgrad<T>(s, SITE_W2_WGRAD, SITE_W2_RED, dZ2, h, (const T*)v.G, f, h, f, Tn, gr[STAGE_W_2]))) return r;
     // dU = (dZ2 W_2) * GELU'(U)
     {
-      GemmArgs g = gemm_args(dZ2, h, p[STAGE_W_2], f, dU, f, Tn, f, h);
+      GemmArgs g = gemm_args(dZ2, h, W2, kBF ? h : f, dU, f, Tn, f, h);
       g.aux = v.U;
       g.ldaux = f;
-      SITE(FFN2_DGRAD, Gemm<T>::run(g, true, false, EPI_DGELU, false, 1, st));
+      SITE(FFN2_DGRAD, Gemm<T>::run(g, true, kBF, EPI_DGELU, false, 1, st));
     }
     if ((r = col_sum<T>(s, SITE_B1_SUM, SITE_B1_RED, dU, f, gr[STAGE_B_1]))) return r;
     // dW_1 = dU^T H1
     if ((r = wgrad<T>(s, SITE_W1_WGRAD, SITE_W1_RED, dU, f, (const T*)v.H1, h, f, h, Tn, gr[STAGE_W_1]))) return r;
     // dH1 = dZ2 + dU W_1
     {
-      GemmArgs g = gemm_args(dU, f, p[STAGE_W_1], h, dH1, h, Tn, h, f);
+      GemmArgs g = gemm_args(dU, f, W1, kBF ? f : h, dH1, h, Tn, h, f);
       g.aux = dZ2;
       g.ldaux = h;
-      SITE(FFN1_DGRAD, Gemm<T>::run(g, true, false, EPI_RESID, false, 1, st));
+      SITE(FFN1_DGRAD, Gemm<T>::run(g, true, kBF, EPI_RESID, false, 1, st));
     }
     // H1 = LN(Z1): dZ1, dgamma1, dbeta1, db_o
     if ((r = ln_backward<T>(s, SITE_LN1_BWD, SITE_LN1_RED, dH1, (const T*)v.xhat1, v.rstd1, (const float*)p[STAGE_G1], dZ1,
@@ -509,8 +535,8 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
     if ((r = wgrad<T>(s, SITE_WO_WGRAD, SITE_WO_RED, dZ1, h, (const T*)v.C, h, h, h, Tn, gr[STAGE_W_O]))) return r;
     // dC = dZ1 W_o
     {
-      GemmArgs g = gemm_args(dZ1, h, p[STAGE_W_O], h, dC, h, Tn, h, h);
-      SITE(OUT_DGRAD, Gemm<T>::run(g, true, false, EPI_STORE, false, 1, st));
+      GemmArgs g = gemm_args(dZ1, h, Wo, h, dC, h, Tn, h, h);
+      SITE(OUT_DGRAD, Gemm<T>::run(g, true, kBF, EPI_STORE, false, 1, st));
     }
     if constexpr (std::is_same<T, bf16_t>::value) {
       AttnArgs aa = attn_args(s, (const bf16_t*)QKV, (bf16_t*)dQKV, v.lse);
@@ -576,10 +602,10 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
     // dX = dZ1 + dQKV W_qkv  (the previous layer's dY, or the stage's dx)
     T* dXout = (l > 0) ? (T*)s->dY : dx;
     {
-      GemmArgs g = gemm_args(dQKV, 3 * h, p[STAGE_W_QKV], h, dXout, h, Tn, h, 3 * h);
+      GemmArgs g = gemm_args(dQKV, 3 * h, Wq, kBF ? 3 * h : h, dXout, h, Tn, h, 3 * h);
       g.aux = dZ1;
       g.ldaux = h;
-      SITE(QKV_DGRAD, Gemm<T>::run(g, true, false, EPI_RESID, false, 1, st));
+      SITE(QKV_DGRAD, Gemm<T>::run(g, true, kBF, EPI_RESID, false, 1, st));
     }
     dYcur = dXout;
   }
