@@ -5,10 +5,9 @@
 // a (BM/2) x (BN/2) sub-tile computed with v_mfma_f32_32x32x16_bf16.  Tiles
 // of A and B are staged in LDS in k-contiguous rows (padded by 8 elements so
 // that the 16-byte fragment reads of 8 consecutive rows hit distinct banks).
-// Operands stored m/n-contiguous in HBM are transposed in registers while
-// being staged (4 k-rows x 8 columns per thread), so every MFMA fragment read
-// is one ds_read_b128 whatever the operand layout.  The next k-tile is
-// fetched into registers while the current one is multiplied.
+// Operands stored m/n-contiguous in HBM keep that layout in LDS and their
+// MFMA fragments are read with gfx950's transposing LDS read.  The next
+// k-tile is fetched into registers while the current one is multiplied.
 #include <type_traits>
 
 #include "kernels.h"
@@ -55,13 +54,18 @@ __device__ __forceinline__ int64_t batch_off(int zb, int zdiv, int64_t s1, int64
 // residual operands are read and the results written as 16-byte row
 // segments.
 // ---------------------------------------------------------------------------
-template <int BM, int BN>
+template <int BM, int BN, bool AK, bool BKM>
 struct TileCfg {
   static constexpr int BK = 64;
-  static constexpr int LDS_LD = BK + 8;  // 144-byte rows: fragment reads of 8 rows hit distinct banks
+  static constexpr int LDS_LD = BK + 8;  // k-major rows: 144 B, fragment reads of 8 rows hit distinct banks
   static constexpr int WM = BM / 2, WN = BN / 2;
   static constexpr int TM = WM / 32, TN = WN / 32;
-  static constexpr int BUF = (BM + BN) * LDS_LD;  // elements per buffer
+  // k-major operand tile: [R][BK + 8]; m/n-major tile: [BK][R + 16] (the
+  // 16-element pad spreads the 4 k-rows a transposing read touches over
+  // distinct banks).
+  static constexpr int A_ELEMS = AK ? BM * LDS_LD : BK * (BM + 16);
+  static constexpr int B_ELEMS = BKM ? BN * LDS_LD : BK * (BN + 16);
+  static constexpr int BUF = A_ELEMS + B_ELEMS;  // elements per buffer
   static constexpr int EPI_LD = WN + 4;          // fp32 staging row
   static constexpr int LDS_BYTES_MAIN = 2 * BUF * 2;
   static constexpr int LDS_BYTES_EPI = 4 * 32 * EPI_LD * 4;
@@ -97,25 +101,21 @@ __device__ __forceinline__ void g2r(__amdgpu_buffer_rsrc_t rs, int64_t ld, int r
       regs[i] = buf_load16(rs, (int)(((int64_t)row * ld + k0 + kc) * 2));
     }
   } else {
-    constexpr int KBN = BK / 4, NBLK = R * BK / 32;
+    constexpr int VPR = R / 8;  // vectors per k-row
 #pragma unroll
-    for (int i = 0; i < (NBLK + NT - 1) / NT; ++i) {
-      const int blk = tid + NT * i;
-      const int kb = blk % KBN, cb = blk / KBN;
-      const int gc = r0 + cb * 8;
-      const bool ok = blk < NBLK && gc < lim;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int gk = k0 + kb * 4 + j;
-        const u32x4_t v = buf_load16(rs, (int)(((int64_t)gk * ld + (ok ? gc : 0)) * 2));
-        regs[4 * i + j] = ok ? v : u32x4_t{0, 0, 0, 0};
-      }
+    for (int i = 0; i < R * BK / 8 / NT; ++i) {
+      const int v = tid + NT * i;
+      const int kr = v / VPR, c8 = (v % VPR) * 8;
+      const int gc = r0 + c8;
+      const bool ok = gc < lim;
+      const u32x4_t x = buf_load16(rs, (int)(((int64_t)(k0 + kr) * ld + (ok ? gc : 0)) * 2));
+      regs[i] = ok ? x : u32x4_t{0, 0, 0, 0};
     }
   }
 }
 
-// Registers -> LDS tile S[R][LDS_LD] (k contiguous).  An m/n-major operand is
-// transposed in registers: 4 k-rows x 8 columns become 8 rows of 4 k.
+// Registers -> LDS: k-major tiles as S[R][LDS_LD], m/n-major tiles as
+// S[BK][R + 16], both plain 16-byte copies.
 template <int R, int BK, int LDS_LD, bool KMAJ>
 __device__ __forceinline__ void r2s(bf16_t* S, const u32x4_t* regs) {
   const int tid = threadIdx.x;
@@ -128,28 +128,44 @@ __device__ __forceinline__ void r2s(bf16_t* S, const u32x4_t* regs) {
       *(u32x4_t*)(S + row * LDS_LD + kc) = regs[i];
     }
   } else {
-    constexpr int KBN = BK / 4, NBLK = R * BK / 32;
+    constexpr int VPR = R / 8;
 #pragma unroll
-    for (int i = 0; i < (NBLK + NT - 1) / NT; ++i) {
-      const int blk = tid + NT * i;
-      if (blk >= NBLK) continue;
-      const int kb = blk % KBN, cb = blk / KBN;
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const int w = c >> 1, sh = (c & 1) * 16;
-        const uint32_t e0 = (regs[4 * i + 0][w] >> sh) & 0xffffu;
-        const uint32_t e1 = (regs[4 * i + 1][w] >> sh) & 0xffffu;
-        const uint32_t e2 = (regs[4 * i + 2][w] >> sh) & 0xffffu;
-        const uint32_t e3 = (regs[4 * i + 3][w] >> sh) & 0xffffu;
-        *(u32x2_t*)(S + (cb * 8 + c) * LDS_LD + kb * 4) = u32x2_t{e0 | (e1 << 16), e2 | (e3 << 16)};
-      }
+    for (int i = 0; i < R * BK / 8 / NT; ++i) {
+      const int v = tid + NT * i;
+      const int kr = v / VPR, c8 = (v % VPR) * 8;
+      *(u32x4_t*)(S + kr * (R + 16) + c8) = regs[i];
     }
   }
 }
 
-template <int R, int BK, bool KMAJ>
+// MFMA fragment (8 consecutive k of one row r0 + lane % 32, k offset
+// ks * 16 + 8 * (lane / 32)) from an LDS tile.  k-major: one 16-byte read.
+// m/n-major [BK][R + 16]: two ds_read_b64_tr_b16.  That instruction works on
+// groups of 16 lanes: lane j supplies the address of 4 consecutive 16-bit
+// values V[j][0..3], and lane i receives V[4e + i / 4][i % 4] for e = 0..3.
+// Lane j of a group points at k-row k0 + j / 4, columns mb + 4 (j % 4), so
+// lane i receives the column mb + i at k-rows k0 .. k0 + 3.
+template <int R, int LDS_LD, bool KMAJ>
+__device__ __forceinline__ bf16x8_t frag(const bf16_t* S, int r0, int ks, int lane) {
+  if constexpr (KMAJ) {
+    return *(const bf16x8_t*)(S + (r0 + (lane & 31)) * LDS_LD + ks * 16 + (lane >> 5) * 8);
+  } else {
+    typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+    const int grp = lane >> 4, j = lane & 15;
+    const int k0 = ks * 16 + 8 * (grp >> 1);
+    const int mb = r0 + 16 * (grp & 1);
+    const bf16_t* p = S + (k0 + (j >> 2)) * (R + 16) + mb + 4 * (j & 3);
+    const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+        (__attribute__((address_space(3))) bf16x4_t*)(p));
+    const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+        (__attribute__((address_space(3))) bf16x4_t*)(p + 4 * (R + 16)));
+    return bf16x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  }
+}
+
+template <int R, int BK>
 constexpr int stage_regs() {
-  return KMAJ ? R * (BK / 8) / NT : 4 * ((R * BK / 32 + NT - 1) / NT);
+  return R * BK / 8 / NT;
 }
 
 __device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
@@ -220,7 +236,7 @@ __device__ __forceinline__ void epi8(const GemmArgs& g, int64_t offC, int zs, in
 
 template <int BM, int BN, bool AK, bool BKM, int EPI, bool OUTF32>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
-  using C = TileCfg<BM, BN>;
+  using C = TileCfg<BM, BN, AK, BKM>;
   constexpr int BK = C::BK, LDS_LD = C::LDS_LD, TM = C::TM, TN = C::TN;
   __shared__ __attribute__((aligned(16))) unsigned char smem_raw[C::LDS_BYTES];
   bf16_t* smem = (bf16_t*)smem_raw;
@@ -240,7 +256,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
   const int wm = wave >> 1, wn = wave & 1;
   const int hf = lane >> 5, rr = lane & 31;
 
-  constexpr int AR = stage_regs<BM, BK, AK>(), BR = stage_regs<BN, BK, BKM>();
+  constexpr int AR = stage_regs<BM, BK>(), BR = stage_regs<BN, BK>();
   u32x4_t ra[AR], rb[BR];
 
   // Buffer resources (see g2r); k offsets passed to g2r are relative to kbeg
@@ -275,13 +291,13 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
     g2r<BM, BK, AK>(rsA, g.lda, m0, g.M, kA0, ra);
     g2r<BN, BK, BKM>(rsB, g.ldb, n0, g.N, kB0, rb);
     r2s<BM, BK, LDS_LD, AK>(smem, ra);
-    r2s<BN, BK, LDS_LD, BKM>(smem + BM * LDS_LD, rb);
+    r2s<BN, BK, LDS_LD, BKM>(smem + C::A_ELEMS, rb);
     __syncthreads();
   }
   constexpr int KS = BK / 16;
   for (int t = 0; t < ntiles; ++t) {
     const bf16_t* As = smem + (t & 1) * C::BUF;
-    const bf16_t* Bs = As + BM * LDS_LD;
+    const bf16_t* Bs = As + C::A_ELEMS;
     const bool more = t + 1 < ntiles;
     if (more) {
       g2r<BM, BK, AK>(rsA, g.lda, m0, g.M, kA0 + (t + 1) * BK, ra);
@@ -290,28 +306,25 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
     // Fragments of k-step ks + 1 are read while the MFMAs of ks run.
     bf16x8_t af[2][TM], bfr[2][TN];
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
-      af[0][i] = *(const bf16x8_t*)(As + (wm * C::WM + i * 32 + rr) * LDS_LD + hf * 8);
+    for (int i = 0; i < TM; ++i) af[0][i] = frag<BM, LDS_LD, AK>(As, wm * C::WM + i * 32, 0, lane);
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
-      bfr[0][j] = *(const bf16x8_t*)(Bs + (wn * C::WN + j * 32 + rr) * LDS_LD + hf * 8);
+    for (int j = 0; j < TN; ++j) bfr[0][j] = frag<BN, LDS_LD, BKM>(Bs, wn * C::WN + j * 32, 0, lane);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const int cur = ks & 1, nxt = cur ^ 1;
       if (ks + 1 < KS) {
-        const int kofs = (ks + 1) * 16 + hf * 8;
 #pragma unroll
         for (int i = 0; i < TM; ++i)
-          af[nxt][i] = *(const bf16x8_t*)(As + (wm * C::WM + i * 32 + rr) * LDS_LD + kofs);
+          af[nxt][i] = frag<BM, LDS_LD, AK>(As, wm * C::WM + i * 32, ks + 1, lane);
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          bfr[nxt][j] = *(const bf16x8_t*)(Bs + (wn * C::WN + j * 32 + rr) * LDS_LD + kofs);
+          bfr[nxt][j] = frag<BN, LDS_LD, BKM>(Bs, wn * C::WN + j * 32, ks + 1, lane);
       }
       if (ks == KS - 1 && more) {
         // The next tile goes to the other buffer while the last MFMAs run.
         bf16_t* An = smem + ((t + 1) & 1) * C::BUF;
         r2s<BM, BK, LDS_LD, AK>(An, ra);
-        r2s<BN, BK, LDS_LD, BKM>(An + BM * LDS_LD, rb);
+        r2s<BN, BK, LDS_LD, BKM>(An + C::A_ELEMS, rb);
       }
       // Keep the scheduler from sinking the fragment reads of ks + 1 down to
       // their uses: they must be in flight while these MFMAs execute.
@@ -518,11 +531,14 @@ hipError_t gemm_bf16(const GemmArgs& g, bool a_kmajor, bool b_kmajor, GemmEpi ep
   if (g.ksplit > 1 && g.kchunk % 64 != 0) return hipErrorInvalidValue;
   if ((a_kmajor || b_kmajor) && g.K % 64 != 0) return hipErrorInvalidValue;
   if ((!a_kmajor && g.M % 8 != 0) || (g.lda % 8 != 0) || (g.ldb % 8 != 0)) return hipErrorInvalidValue;
-  const int64_t t256 = (int64_t)((g.M + 255) / 256) * ((g.N + 255) / 256) * batch * g.ksplit;
-  if (t256 >= 512) return dispatch_layout<256, 256>(g, a_kmajor, b_kmajor, epi, out_f32, batch, st);
-  if (g.N <= 128 || t256 < 128)
-    return dispatch_layout<128, 128>(g, a_kmajor, b_kmajor, epi, out_f32, batch, st);
-  return dispatch_layout<256, 128>(g, a_kmajor, b_kmajor, epi, out_f32, batch, st);
+  int tile = g.tile;
+  if (tile == 0) {
+    const int64_t t256 = (int64_t)((g.M + 255) / 256) * ((g.N + 255) / 256) * batch * g.ksplit;
+    tile = (g.M >= 256 && g.N >= 256 && t256 >= 192) ? 1 : (g.N > 128 && t256 >= 64 ? 2 : 3);
+  }
+  if (tile == 1) return dispatch_layout<256, 256>(g, a_kmajor, b_kmajor, epi, out_f32, batch, st);
+  if (tile == 2) return dispatch_layout<256, 128>(g, a_kmajor, b_kmajor, epi, out_f32, batch, st);
+  return dispatch_layout<128, 128>(g, a_kmajor, b_kmajor, epi, out_f32, batch, st);
 }
 
 hipError_t gemm_f32(const GemmArgs& g, bool a_kmajor, bool b_kmajor, GemmEpi epi, int batch,

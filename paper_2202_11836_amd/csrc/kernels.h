@@ -38,6 +38,7 @@ struct GemmArgs {
   int ksplit;
   int kchunk;
   float alpha;
+  int tile;  // bf16 tile shape: 0 = automatic, 1 = 256x256, 2 = 256x128, 3 = 128x128
 };
 
 inline GemmArgs gemm_args(const void* A, int64_t lda, const void* B, int64_t ldb, void* C,

@@ -243,12 +243,23 @@ stage_status dev_alloc(stage_t* s, std::vector<void*>& list, void** p, size_t by
   return STAGE_OK;
 }
 
-// Number of K splits for a weight-gradient GEMM with reduction length K over
-// `tiles` output tiles: enough work-groups to cover the chip, chunks of at
-// least 256 rows.
-int choose_ksplit(int64_t tiles, int K) {
-  int ks = 1;
-  while (tiles * ks < 512 && K / (ks * 2) >= 256 && ks < 32) ks *= 2;
+// Tiling of a weight-gradient GEMM dW[M, N] = sum over K = T tokens: the
+// output has few tiles, so the token range is split until about one
+// work-group per CU (256) is running.  256x256 tiles when the output has at
+// least 16 of them, else 128x128.  Returns the split count; *tile receives
+// the GemmArgs tile code.
+int wgrad_split(int64_t M, int64_t N, int K, int* tile) {
+  const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256);
+  int64_t tiles;
+  if (t256 >= 16) {
+    *tile = 1;
+    tiles = t256;
+  } else {
+    *tile = 3;
+    tiles = ((M + 127) / 128) * ((N + 127) / 128);
+  }
+  int ks = (int)std::max<int64_t>(1, 256 / tiles);
+  ks = std::min(ks, std::max(1, K / 512));  // chunks of at least 512 tokens
   return ks;
 }
 
@@ -293,8 +304,8 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
   size_t need = 0;
   const int64_t shapes[4][2] = {{3 * h, h}, {h, h}, {f, h}, {h, f}};
   for (auto& mn : shapes) {
-    int64_t tiles = ((mn[0] + 127) / 128) * ((mn[1] + 127) / 128);
-    int ks = choose_ksplit(tiles, (int)T);
+    int tile;
+    int ks = wgrad_split(mn[0], mn[1], (int)T, &tile);
     if (ks > 1) need = std::max<size_t>(need, (size_t)ks * mn[0] * mn[1]);
   }
   s->splitk_elems = need;
@@ -328,8 +339,7 @@ template <typename T>
 stage_status wgrad(stage_t* s, int site, int site_red, const T* dYm, int64_t ld_dy, const T* Xn,
                    int64_t ld_x, int M, int N, int Tk, float* out) {
   GemmArgs g = gemm_args(dYm, ld_dy, Xn, ld_x, out, N, M, N, Tk);
-  int64_t tiles = (int64_t)((M + 127) / 128) * ((N + 127) / 128);
-  int ks = choose_ksplit(tiles, Tk);
+  int ks = wgrad_split(M, N, Tk, &g.tile);
   if (ks > 1 && (size_t)ks * M * N <= s->splitk_elems) {
     int chunk = (Tk + ks - 1) / ks;
     chunk = (chunk + 63) / 64 * 64;
