@@ -25,6 +25,18 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2516.6  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 
+# Kernels the roofline entry can report on: a kernel (one compiled
+# instantiation) and the launch sites that use it in one step.
+ROOFLINE_KERNELS = {
+    # weight-gradient GEMM dW = dY^T X over all tokens (split over tokens,
+    # fp32 partials): the kernel with the largest share of step time
+    "wgrad_gemm": ("gemm_bf16_kernel<256, 256, false, false, 4, true>",
+                   ["w2_wgrad_gemm", "w1_wgrad_gemm", "wo_wgrad_gemm", "wqkv_wgrad_gemm"]),
+    "ffn1_gelu_gemm": ("gemm_bf16_kernel<256, 256, true, true, 1, false>", ["ffn1_gelu_gemm_fwd"]),
+    "ffn2_dgrad_dgelu_gemm": ("gemm_bf16_kernel<256, 256, true, true, 2, false>",
+                              ["ffn2_dgrad_dgelu_gemm"]),
+}
+
 
 def site_flops(site: str, cfg, lengths) -> float:
     """Algorithmic FLOPs of one launch of a GEMM site (2 M N K)."""
@@ -48,6 +60,24 @@ def site_flops(site: str, cfg, lengths) -> float:
               "dk_gemm_bwd"):
         table[k] = 2.0 * cfg.batch * H * S * S * 64
     return table.get(site, 0.0)
+
+
+def roofline_traffic(key: str, kernel_name: str):
+    """HBM bytes per launch of the roofline kernel from the rocprofv3 --pmc
+    record under profiles/ (FETCH_SIZE and WRITE_SIZE, scaled by a plain copy
+    of known size), or None when no record exists or the GEMM source changed
+    since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "roofline_traffic.json")
+    src = os.path.join(ROOT, "paper_2202_11836_amd", "csrc", "gemm.hip")
+    try:
+        rec = json.load(open(path)).get(key)
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("kernel") != kernel_name or rec.get("source_sha256") != sha:
+        return None
+    return rec["bytes_per_launch"]
 
 
 def cpu_baseline(cfg, budget_s: float = 10.0):
@@ -86,10 +116,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="bert_large_4")
     ap.add_argument("--layers", type=int, default=None, help="override L (depth sweep)")
-    ap.add_argument("--roofline-site", default="ffn1_gelu_gemm_fwd")
+    ap.add_argument("--roofline-kernel", default="wgrad_gemm", choices=sorted(ROOFLINE_KERNELS))
     ap.add_argument("--breakdown", action="store_true", help="per-site times to stderr")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="after timing, copy a fresh buffer of this size once (the known-size "
+                         "copy that scales rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -139,7 +172,8 @@ def main():
 
     # Timed region; the dominant kernel's launches are traced with HIP events
     # on the stage stream.
-    st.trace(args.roofline_site)
+    kernel_name, roof_sites = ROOFLINE_KERNELS[args.roofline_kernel]
+    st.trace(roof_sites)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -154,9 +188,12 @@ def main():
     flops = synth.flops_per_step(cfg, inp["lengths"] if cfg.len_lo is not None else None)
     tflops = flops / (ms_per_step / 1000.0) / 1e12
 
-    per_launch_flops = site_flops(args.roofline_site, cfg, inp["lengths"])
+    # Algorithmic FLOPs per launch: 2 M N K of each traced launch in a step,
+    # averaged over the step's launches of the kernel.
+    per_launch_flops = sum(site_flops(s, cfg, inp["lengths"]) for s in roof_sites) / len(roof_sites)
     avg_ms = site_ms / max(launches, 1)
     achieved = per_launch_flops / (avg_ms / 1000.0) / 1e12 if launches else 0.0
+    traffic = roofline_traffic(args.roofline_kernel, kernel_name)
 
     if args.breakdown:
         rows = []
@@ -202,19 +239,28 @@ def main():
             "global_batch": cfg.batch, "seq_len": cfg.seq, "gflop_per_step": flops / 1e9,
         },
         "roofline": {
-            "kernel": args.roofline_site,
+            "kernel": kernel_name,
+            "sites": roof_sites,
             "bound": "mfma",
             "achieved": achieved,
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_BF16_TFLOPS,
-            "traffic": None,
+            "traffic": traffic,
             "launches": launches,
             "avg_launch_ms": avg_ms,
             "flop_per_launch": per_launch_flops,
         },
     }
     st.close()
+    if args.calibrate_copy_mib > 0:
+        n = args.calibrate_copy_mib * (1 << 20) // 4
+        src = torch.arange(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_budget)
     print(json.dumps(out), flush=True)

@@ -151,6 +151,8 @@ size_t stage_tensor_bytes(stage_t* s, int kind, int layer, int which);
  * to untraced ones.
  */
 stage_status stage_trace_site(stage_t* s, int site);
+/* Same for a set of sites: bit i of mask selects site i (0 = off). */
+stage_status stage_trace_mask(stage_t* s, uint64_t mask);
 stage_status stage_trace_read(stage_t* s, int* launches, double* total_ms);
 int stage_site_count(void);
 const char* stage_site_name(int site); /* "" for an unknown site */

@@ -24,7 +24,8 @@ STATUS_NAMES = {0: "OK", 1: "EINVAL", 2: "ESTATE", 3: "ENOMEM", 4: "EHIP"}
 
 EXPORTED = ("stage_init", "stage_set_stream", "stage_forward", "stage_backward", "stage_param",
             "stage_grad", "stage_set_param", "stage_read", "stage_tensor_bytes",
-            "stage_trace_site", "stage_trace_read", "stage_site_count", "stage_site_name",
+            "stage_trace_site", "stage_trace_mask", "stage_trace_read", "stage_site_count",
+            "stage_site_name",
             "stage_last_error", "stage_destroy")
 
 _lib = None
@@ -69,6 +70,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.stage_tensor_bytes.restype = sz
     lib.stage_trace_site.argtypes = [vp, i32]
     lib.stage_trace_site.restype = i32
+    lib.stage_trace_mask.argtypes = [vp, u64]
+    lib.stage_trace_mask.restype = i32
     lib.stage_trace_read.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]
     lib.stage_trace_read.restype = i32
     lib.stage_site_count.argtypes = []
@@ -157,6 +160,10 @@ def stage_tensor_bytes(handle, kind: int, layer: int, which: int) -> int:
 
 def stage_trace_site(handle, site: int) -> None:
     _check(handle, load_library().stage_trace_site(handle, site))
+
+
+def stage_trace_mask(handle, mask: int) -> None:
+    _check(handle, load_library().stage_trace_mask(handle, mask))
 
 
 def stage_trace_read(handle):
@@ -260,14 +267,18 @@ class Stage:
         stage_read(self.handle, KIND_SAVED, layer, which, out)
         return out
 
-    def trace(self, site_name: Optional[str]):
-        """Trace every launch of the named kernel site (None: off)."""
-        site = -1
-        if site_name is not None:
-            names = [stage_site_name(i) for i in range(stage_site_count())]
-            site = names.index(site_name)
+    def trace(self, site_names):
+        """Trace every launch of the named kernel site(s) (None: off)."""
+        if site_names is None:
+            site_names = []
+        elif isinstance(site_names, str):
+            site_names = [site_names]
+        names = [stage_site_name(i) for i in range(stage_site_count())]
+        mask = 0
+        for n in site_names:
+            mask |= 1 << names.index(n)
         self._sync_stream()
-        stage_trace_site(self.handle, site)
+        stage_trace_mask(self.handle, mask)
 
     def trace_read(self):
         """(launches, total_ms) of the traced site since trace() / the last read."""

@@ -149,8 +149,8 @@ struct stage {
   bool have_ctx = false;
   std::string err;
 
-  // Event tracing of one launch site.
-  int trace_site = -1;
+  // Event tracing of a set of launch sites (bit i = site i).
+  uint64_t trace_mask = 0;
   std::vector<hipEvent_t> events;  // pool, reused
   size_t events_used = 0;
 };
@@ -175,7 +175,7 @@ stage_status fail(stage_t* s, stage_status st, const std::string& msg) {
 // Records a start event before a traced site's launch; returns the pool
 // index of the event pair, or -1 when the site is not traced.
 int trace_begin(stage_t* s, int site) {
-  if (s->trace_site != site) return -1;
+  if (!((s->trace_mask >> site) & 1)) return -1;
   while (s->events.size() < s->events_used + 2) {
     hipEvent_t e;
     if (hipEventCreate(&e) != hipSuccess) return -1;
@@ -851,7 +851,13 @@ stage_status stage_read(stage_t* s, int kind, int layer, int which, void* dst, s
 stage_status stage_trace_site(stage_t* s, int site) {
   if (!s) return STAGE_EINVAL;
   if (site < -1 || site >= SITE_COUNT) return fail(s, STAGE_EINVAL, "unknown site");
-  s->trace_site = site;
+  return stage_trace_mask(s, site < 0 ? 0 : (uint64_t)1 << site);
+}
+
+stage_status stage_trace_mask(stage_t* s, uint64_t mask) {
+  if (!s) return STAGE_EINVAL;
+  if (SITE_COUNT < 64 && (mask >> SITE_COUNT) != 0) return fail(s, STAGE_EINVAL, "unknown site");
+  s->trace_mask = mask;
   s->events_used = 0;
   return STAGE_OK;
 }
