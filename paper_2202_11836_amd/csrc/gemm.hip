@@ -2,12 +2,12 @@
 // and an fp32 vector-ALU GEMM, both with fused epilogues.
 //
 // bf16 path: 256 threads = 4 wavefronts in a 2 x 2 grid; each wavefront owns
-// a (BM/2) x (BN/2) sub-tile computed with v_mfma_f32_32x32x16_bf16.  Tiles
-// of A and B are staged in LDS in k-contiguous rows (padded by 8 elements so
-// that the 16-byte fragment reads of 8 consecutive rows hit distinct banks).
-// Operands stored m/n-contiguous in HBM keep that layout in LDS and their
-// MFMA fragments are read with gfx950's transposing LDS read.  The next
-// k-tile is fetched into registers while the current one is multiplied.
+// a (BM/2) x (BN/2) sub-tile computed with v_mfma_f32_32x32x16_bf16.  k-tiles
+// of 64 go straight from HBM into a 2-stage LDS ring with direct-to-LDS
+// buffer loads, issued one k-tile ahead, so no staging registers and no LDS
+// store instructions sit in the main loop.  Operands stored m/n-contiguous in
+// HBM keep that layout in LDS and their MFMA fragments are read with gfx950's
+// transposing LDS read.
 #include <type_traits>
 
 #include "kernels.h"
@@ -57,17 +57,12 @@ __device__ __forceinline__ int64_t batch_off(int zb, int zdiv, int64_t s1, int64
 template <int BM, int BN, bool AK, bool BKM>
 struct TileCfg {
   static constexpr int BK = 64;
-  static constexpr int LDS_LD = BK + 8;  // k-major rows: 144 B, fragment reads of 8 rows hit distinct banks
   static constexpr int WM = BM / 2, WN = BN / 2;
   static constexpr int TM = WM / 32, TN = WN / 32;
-  // k-major operand tile: [R][BK + 8]; m/n-major tile: [BK][R + 16] (the
-  // 16-element pad spreads the 4 k-rows a transposing read touches over
-  // distinct banks).
-  static constexpr int A_ELEMS = AK ? BM * LDS_LD : BK * (BM + 16);
-  static constexpr int B_ELEMS = BKM ? BN * LDS_LD : BK * (BN + 16);
-  static constexpr int BUF = A_ELEMS + B_ELEMS;  // elements per buffer
-  static constexpr int EPI_LD = WN + 4;          // fp32 staging row
-  static constexpr int LDS_BYTES_MAIN = 2 * BUF * 2;
+  static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
+  static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+  static constexpr int EPI_LD = WN + 4;  // fp32 staging row
+  static constexpr int LDS_BYTES_MAIN = 2 * STAGE_BYTES;
   static constexpr int LDS_BYTES_EPI = 4 * 32 * EPI_LD * 4;
   static constexpr int LDS_BYTES = LDS_BYTES_MAIN > LDS_BYTES_EPI ? LDS_BYTES_MAIN : LDS_BYTES_EPI;
 };
@@ -78,94 +73,70 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, in
   return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, nrec, 0x00020000);
 }
 
-__device__ __forceinline__ u32x4_t buf_load16(__amdgpu_buffer_rsrc_t r, int byte_off) {
-  return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0));
-}
+typedef __attribute__((address_space(3))) void lds_void_t;
 
-// Global -> registers for one operand tile of k-tile k0 (relative to the
-// resource's first k).  k-major: the resource starts at the tile's first
-// row and ends at the operand's last valid row, so rows past it read 0 (K is
-// a multiple of BK for k-major operands).  m/n-major: the resource spans this
-// split's k rows [kbeg, K), so k rows past K read 0; columns past lim are
-// zeroed by a select.
-template <int R, int BK, bool KMAJ>
-__device__ __forceinline__ void g2r(__amdgpu_buffer_rsrc_t rs, int64_t ld, int r0, int lim, int k0,
-                                    u32x4_t* regs) {
-  const int tid = threadIdx.x;
-  if constexpr (KMAJ) {
-    constexpr int VPR = BK / 8;
+// LDS tile layouts (no padding; 16-byte chunks XOR-swizzled so that the
+// fragment reads of one pass hit distinct banks):
+//   k-major  [R][64]: row r, logical chunk c (8 k values) at physical chunk
+//            c ^ ((r >> 1) & 7) of the row's 128 bytes;
+//   m/n-major [64][R]: k-row k, logical chunk c (8 rows/columns) at physical
+//            chunk c ^ (2 (k & 3)) of the row's 2R bytes.
+//
+// dma_tile issues the direct-to-LDS loads (buffer_load ... lds, 16 bytes per
+// lane; lane l of a load lands at LDS base + 16 l) that fill one operand tile
+// of k-tile k0 (k relative to the resource, see the kernel), so the tile
+// never passes through VGPRs.  Each 1 KB block is one instruction; the 4
+// wavefronts split the blocks.
+template <int R, bool KMAJ>
+__device__ __forceinline__ void dma_tile(__amdgpu_buffer_rsrc_t rs, int64_t ld, int k0, char* dst,
+                                         int wave, int lane) {
+  constexpr int NB = R * 64 * 2 / 1024;  // 1 KB blocks in the tile
 #pragma unroll
-    for (int i = 0; i < R * VPR / NT; ++i) {
-      const int v = tid + NT * i;
-      const int row = v / VPR, kc = (v % VPR) * 8;
-      regs[i] = buf_load16(rs, (int)(((int64_t)row * ld + k0 + kc) * 2));
+  for (int i = 0; i < NB / 4; ++i) {
+    const int q = wave * (NB / 4) + i;
+    int64_t elem;
+    if constexpr (KMAJ) {
+      const int row = 8 * q + (lane >> 3);
+      const int c = (lane & 7) ^ ((row >> 1) & 7);
+      elem = (int64_t)row * ld + k0 + 8 * c;
+    } else {
+      constexpr int CPR = R / 8;           // chunks per k-row
+      constexpr int KPB = 64 / CPR;        // k-rows per block
+      const int kr = KPB * q + lane / CPR;
+      const int c = (lane % CPR) ^ (2 * (kr & 3));
+      elem = (int64_t)(k0 + kr) * ld + 8 * c;
     }
-  } else {
-    constexpr int VPR = R / 8;  // vectors per k-row
-#pragma unroll
-    for (int i = 0; i < R * BK / 8 / NT; ++i) {
-      const int v = tid + NT * i;
-      const int kr = v / VPR, c8 = (v % VPR) * 8;
-      const int gc = r0 + c8;
-      const bool ok = gc < lim;
-      const u32x4_t x = buf_load16(rs, (int)(((int64_t)(k0 + kr) * ld + (ok ? gc : 0)) * 2));
-      regs[i] = ok ? x : u32x4_t{0, 0, 0, 0};
-    }
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)(dst + q * 1024), 16, (int)(elem * 2),
+                                             0, 0, 0);
   }
 }
 
-// Registers -> LDS: k-major tiles as S[R][LDS_LD], m/n-major tiles as
-// S[BK][R + 16], both plain 16-byte copies.
-template <int R, int BK, int LDS_LD, bool KMAJ>
-__device__ __forceinline__ void r2s(bf16_t* S, const u32x4_t* regs) {
-  const int tid = threadIdx.x;
+// MFMA operand fragment: 8 consecutive k (offset ks * 16 + 8 * (lane / 32)) of
+// row r0 + lane % 32.  k-major: one 16-byte read.  m/n-major: two
+// ds_read_b64_tr_b16.  That instruction works on groups of 16 lanes: lane j
+// supplies the address of 4 consecutive 16-bit values V[j][0..3], and lane i
+// receives V[4e + i / 4][i % 4] for e = 0..3.  Lane j of a group points at
+// k-row k0 + j / 4, columns mb + 4 (j % 4), so lane i receives column mb + i
+// at k-rows k0 .. k0 + 3 (the second read: k0 + 4 .. k0 + 7).
+template <int R, bool KMAJ>
+__device__ __forceinline__ bf16x8_t frag(const char* S, int r0, int ks, int lane) {
   if constexpr (KMAJ) {
-    constexpr int VPR = BK / 8;
-#pragma unroll
-    for (int i = 0; i < R * VPR / NT; ++i) {
-      const int v = tid + NT * i;
-      const int row = v / VPR, kc = (v % VPR) * 8;
-      *(u32x4_t*)(S + row * LDS_LD + kc) = regs[i];
-    }
-  } else {
-    constexpr int VPR = R / 8;
-#pragma unroll
-    for (int i = 0; i < R * BK / 8 / NT; ++i) {
-      const int v = tid + NT * i;
-      const int kr = v / VPR, c8 = (v % VPR) * 8;
-      *(u32x4_t*)(S + kr * (R + 16) + c8) = regs[i];
-    }
-  }
-}
-
-// MFMA fragment (8 consecutive k of one row r0 + lane % 32, k offset
-// ks * 16 + 8 * (lane / 32)) from an LDS tile.  k-major: one 16-byte read.
-// m/n-major [BK][R + 16]: two ds_read_b64_tr_b16.  That instruction works on
-// groups of 16 lanes: lane j supplies the address of 4 consecutive 16-bit
-// values V[j][0..3], and lane i receives V[4e + i / 4][i % 4] for e = 0..3.
-// Lane j of a group points at k-row k0 + j / 4, columns mb + 4 (j % 4), so
-// lane i receives the column mb + i at k-rows k0 .. k0 + 3.
-template <int R, int LDS_LD, bool KMAJ>
-__device__ __forceinline__ bf16x8_t frag(const bf16_t* S, int r0, int ks, int lane) {
-  if constexpr (KMAJ) {
-    return *(const bf16x8_t*)(S + (r0 + (lane & 31)) * LDS_LD + ks * 16 + (lane >> 5) * 8);
+    const int r = r0 + (lane & 31);
+    const int c = 2 * ks + (lane >> 5);
+    return *(const bf16x8_t*)(S + r * 128 + 16 * (c ^ ((r >> 1) & 7)));
   } else {
     typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
     const int grp = lane >> 4, j = lane & 15;
-    const int k0 = ks * 16 + 8 * (grp >> 1);
-    const int mb = r0 + 16 * (grp & 1);
-    const bf16_t* p = S + (k0 + (j >> 2)) * (R + 16) + mb + 4 * (j & 3);
+    const int kr = ks * 16 + 8 * (grp >> 1) + (j >> 2);
+    const int col = r0 + 16 * (grp & 1) + 4 * (j & 3);
+    const int off = 16 * ((col >> 3) ^ (2 * (kr & 3))) + 2 * (col & 7);
+    const char* p = S + kr * (2 * R) + off;
     const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
         (__attribute__((address_space(3))) bf16x4_t*)(p));
     const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-        (__attribute__((address_space(3))) bf16x4_t*)(p + 4 * (R + 16)));
+        (__attribute__((address_space(3))) bf16x4_t*)(p + 4 * (2 * R)));
     return bf16x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
   }
-}
-
-template <int R, int BK>
-constexpr int stage_regs() {
-  return R * BK / 8 / NT;
 }
 
 __device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
@@ -237,9 +208,8 @@ __device__ __forceinline__ void epi8(const GemmArgs& g, int64_t offC, int zs, in
 template <int BM, int BN, bool AK, bool BKM, int EPI, bool OUTF32>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
   using C = TileCfg<BM, BN, AK, BKM>;
-  constexpr int BK = C::BK, LDS_LD = C::LDS_LD, TM = C::TM, TN = C::TN;
-  __shared__ __attribute__((aligned(16))) unsigned char smem_raw[C::LDS_BYTES];
-  bf16_t* smem = (bf16_t*)smem_raw;
+  constexpr int BK = C::BK, TM = C::TM, TN = C::TN;
+  __shared__ __attribute__((aligned(1024))) char smem[C::LDS_BYTES];
 
   const int nbm = (g.M + BM - 1) / BM, nbn = (g.N + BN - 1) / BN;
   int tm, tn;
@@ -256,25 +226,25 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
   const int wm = wave >> 1, wn = wave & 1;
   const int hf = lane >> 5, rr = lane & 31;
 
-  constexpr int AR = stage_regs<BM, BK>(), BR = stage_regs<BN, BK>();
-  u32x4_t ra[AR], rb[BR];
-
-  // Buffer resources (see g2r); k offsets passed to g2r are relative to kbeg
-  // for m/n-major operands and absolute for k-major ones.
+  // Buffer resources.  k-major: from the tile's first row to the operand's
+  // last row (rows past it read 0; K is a multiple of 64).  m/n-major: from
+  // this split's first k-row and the tile's first column to the end of the
+  // operand (k-rows past K read 0).  Reads past the valid columns of a
+  // m/n-major row only feed output rows/columns that are never stored.
   __amdgpu_buffer_rsrc_t rsA, rsB;
   int kA0, kB0;
   if constexpr (AK) {
     rsA = make_rsrc(A + (int64_t)m0 * g.lda, (int64_t)(g.M - m0) * g.lda * 2);
     kA0 = kbeg;
   } else {
-    rsA = make_rsrc(A + (int64_t)kbeg * g.lda, (int64_t)(g.K - kbeg) * g.lda * 2);
+    rsA = make_rsrc(A + (int64_t)kbeg * g.lda + m0, ((int64_t)(g.K - kbeg) * g.lda - m0) * 2);
     kA0 = 0;
   }
   if constexpr (BKM) {
     rsB = make_rsrc(B + (int64_t)n0 * g.ldb, (int64_t)(g.N - n0) * g.ldb * 2);
     kB0 = kbeg;
   } else {
-    rsB = make_rsrc(B + (int64_t)kbeg * g.ldb, (int64_t)(g.K - kbeg) * g.ldb * 2);
+    rsB = make_rsrc(B + (int64_t)kbeg * g.ldb + n0, ((int64_t)(g.K - kbeg) * g.ldb - n0) * 2);
     kB0 = 0;
   }
 
@@ -287,44 +257,38 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   const int ntiles = (kend - kbeg + BK - 1) / BK;
-  if (ntiles > 0) {
-    g2r<BM, BK, AK>(rsA, g.lda, m0, g.M, kA0, ra);
-    g2r<BN, BK, BKM>(rsB, g.ldb, n0, g.N, kB0, rb);
-    r2s<BM, BK, LDS_LD, AK>(smem, ra);
-    r2s<BN, BK, LDS_LD, BKM>(smem + C::A_ELEMS, rb);
-    __syncthreads();
-  }
   constexpr int KS = BK / 16;
+  if (ntiles > 0) {
+    dma_tile<BM, AK>(rsA, g.lda, kA0, smem, wave, lane);
+    dma_tile<BN, BKM>(rsB, g.ldb, kB0, smem + C::A_BYTES, wave, lane);
+  }
   for (int t = 0; t < ntiles; ++t) {
-    const bf16_t* As = smem + (t & 1) * C::BUF;
-    const bf16_t* Bs = As + C::A_ELEMS;
-    const bool more = t + 1 < ntiles;
-    if (more) {
-      g2r<BM, BK, AK>(rsA, g.lda, m0, g.M, kA0 + (t + 1) * BK, ra);
-      g2r<BN, BK, BKM>(rsB, g.ldb, n0, g.N, kB0 + (t + 1) * BK, rb);
+    // This wavefront's loads of tile t are done (only they are in flight);
+    // the barrier makes every wavefront's loads visible and guarantees that
+    // all wavefronts finished tile t - 1, whose buffer is refilled next.
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    __syncthreads();
+    if (t + 1 < ntiles) {
+      char* nb = smem + ((t + 1) & 1) * C::STAGE_BYTES;
+      dma_tile<BM, AK>(rsA, g.lda, kA0 + (t + 1) * BK, nb, wave, lane);
+      dma_tile<BN, BKM>(rsB, g.ldb, kB0 + (t + 1) * BK, nb + C::A_BYTES, wave, lane);
     }
+    const char* As = smem + (t & 1) * C::STAGE_BYTES;
+    const char* Bs = As + C::A_BYTES;
     // Fragments of k-step ks + 1 are read while the MFMAs of ks run.
     bf16x8_t af[2][TM], bfr[2][TN];
 #pragma unroll
-    for (int i = 0; i < TM; ++i) af[0][i] = frag<BM, LDS_LD, AK>(As, wm * C::WM + i * 32, 0, lane);
+    for (int i = 0; i < TM; ++i) af[0][i] = frag<BM, AK>(As, wm * C::WM + i * 32, 0, lane);
 #pragma unroll
-    for (int j = 0; j < TN; ++j) bfr[0][j] = frag<BN, LDS_LD, BKM>(Bs, wn * C::WN + j * 32, 0, lane);
+    for (int j = 0; j < TN; ++j) bfr[0][j] = frag<BN, BKM>(Bs, wn * C::WN + j * 32, 0, lane);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const int cur = ks & 1, nxt = cur ^ 1;
       if (ks + 1 < KS) {
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
-          af[nxt][i] = frag<BM, LDS_LD, AK>(As, wm * C::WM + i * 32, ks + 1, lane);
+        for (int i = 0; i < TM; ++i) af[nxt][i] = frag<BM, AK>(As, wm * C::WM + i * 32, ks + 1, lane);
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-          bfr[nxt][j] = frag<BN, LDS_LD, BKM>(Bs, wn * C::WN + j * 32, ks + 1, lane);
-      }
-      if (ks == KS - 1 && more) {
-        // The next tile goes to the other buffer while the last MFMAs run.
-        bf16_t* An = smem + ((t + 1) & 1) * C::BUF;
-        r2s<BM, BK, LDS_LD, AK>(An, ra);
-        r2s<BN, BK, LDS_LD, BKM>(An + C::A_ELEMS, rb);
+        for (int j = 0; j < TN; ++j) bfr[nxt][j] = frag<BN, BKM>(Bs, wn * C::WN + j * 32, ks + 1, lane);
       }
       // Keep the scheduler from sinking the fragment reads of ks + 1 down to
       // their uses: they must be in flight while these MFMAs execute.
@@ -337,13 +301,13 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
               __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
-    __syncthreads();
   }
+  __syncthreads();  // the epilogue reuses the LDS
 
   // Epilogue.  32x32 accumulator layout: lane holds column (lane % 32);
   // register r holds row 8 * (r / 4) + 4 * (lane / 32) + (r % 4).
   const int64_t offC = batch_off(zb, g.zdiv, g.sC1, g.sC2);
-  float* stg = (float*)smem_raw + wave * 32 * C::EPI_LD;
+  float* stg = (float*)smem + wave * 32 * C::EPI_LD;
   const int mw = m0 + wm * C::WM, nw = n0 + wn * C::WN;
   constexpr int CH = C::WN / 8;  // 8-column chunks per staged row
 #pragma unroll
