@@ -4,8 +4,9 @@
 // bf16 path: 256 threads = 4 wavefronts in a 2 x 2 grid; each wavefront owns
 // a (BM/2) x (BN/2) sub-tile computed with v_mfma_f32_32x32x16_bf16.  k-tiles
 // of 64 go straight from HBM into a 2-stage LDS ring with direct-to-LDS
-// buffer loads, issued one k-tile ahead, so no staging registers and no LDS
-// store instructions sit in the main loop.  Operands stored m/n-contiguous in
+// buffer loads, issued a k-tile and a k-step ahead, so no staging registers
+// and no LDS store instructions sit in the main loop, and the one barrier per
+// k-tile overlaps the MFMAs of the last k-step.  Operands stored m/n-contiguous in
 // HBM keep that layout in LDS and their MFMA fragments are read with gfx950's
 // transposing LDS read.
 #include <type_traits>
@@ -80,7 +81,9 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 //   k-major  [R][64]: row r, logical chunk c (8 k values) at physical chunk
 //            c ^ ((r >> 1) & 7) of the row's 128 bytes;
 //   m/n-major [64][R]: k-row k, logical chunk c (8 rows/columns) at physical
-//            chunk c ^ (2 (k & 3)) of the row's 2R bytes.
+//            chunk c ^ (4 (k & 3)) of the row's 2R bytes (R >= 128), so the
+//            4 k-rows x 2 chunks of each 16-lane transposing read, and the two
+//            groups of a 32-lane pass, cover 16 distinct chunks.
 //
 // dma_tile issues the direct-to-LDS loads (buffer_load ... lds, 16 bytes per
 // lane; lane l of a load lands at LDS base + 16 l) that fill one operand tile
@@ -103,7 +106,7 @@ __device__ __forceinline__ void dma_tile(__amdgpu_buffer_rsrc_t rs, int64_t ld, 
       constexpr int CPR = R / 8;           // chunks per k-row
       constexpr int KPB = 64 / CPR;        // k-rows per block
       const int kr = KPB * q + lane / CPR;
-      const int c = (lane % CPR) ^ (2 * (kr & 3));
+      const int c = (lane % CPR) ^ (4 * (kr & 3));
       elem = (int64_t)(k0 + kr) * ld + 8 * c;
     }
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)(dst + q * 1024), 16, (int)(elem * 2),
@@ -129,7 +132,7 @@ __device__ __forceinline__ bf16x8_t frag(const char* S, int r0, int ks, int lane
     const int grp = lane >> 4, j = lane & 15;
     const int kr = ks * 16 + 8 * (grp >> 1) + (j >> 2);
     const int col = r0 + 16 * (grp & 1) + 4 * (j & 3);
-    const int off = 16 * ((col >> 3) ^ (2 * (kr & 3))) + 2 * (col & 7);
+    const int off = 16 * ((col >> 3) ^ (4 * (kr & 3))) + 2 * (col & 7);
     const char* p = S + kr * (2 * R) + off;
     const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
         (__attribute__((address_space(3))) bf16x4_t*)(p));
@@ -258,29 +261,40 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
 
   const int ntiles = (kend - kbeg + BK - 1) / BK;
   constexpr int KS = BK / 16;
+  // s_waitcnt immediates (gfx9 encoding: vmcnt[3:0] | expcnt[6:4] |
+  // lgkmcnt[11:8] | vmcnt[5:4] << 14): "vmcnt <= one k-tile of this
+  // wavefront's direct-to-LDS loads" and "vmcnt = 0 and lgkmcnt = 0".
+  constexpr int NDMA = BM / 32 + BN / 32;
+  constexpr int WAIT_ONE_TILE_IN_FLIGHT = (NDMA & 15) | ((NDMA >> 4) << 14) | 0x0F70;
+  constexpr int WAIT_ALL = 0x0070;
+
+  // Prologue: tiles 0 and 1 in flight, wait for tile 0.
+  bf16x8_t af[2][TM], bfr[2][TN];
   if (ntiles > 0) {
     dma_tile<BM, AK>(rsA, g.lda, kA0, smem, wave, lane);
     dma_tile<BN, BKM>(rsB, g.ldb, kB0, smem + C::A_BYTES, wave, lane);
-  }
-  for (int t = 0; t < ntiles; ++t) {
-    // This wavefront's loads of tile t are done (only they are in flight);
-    // the barrier makes every wavefront's loads visible and guarantees that
-    // all wavefronts finished tile t - 1, whose buffer is refilled next.
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
-    __syncthreads();
-    if (t + 1 < ntiles) {
-      char* nb = smem + ((t + 1) & 1) * C::STAGE_BYTES;
-      dma_tile<BM, AK>(rsA, g.lda, kA0 + (t + 1) * BK, nb, wave, lane);
-      dma_tile<BN, BKM>(rsB, g.ldb, kB0 + (t + 1) * BK, nb + C::A_BYTES, wave, lane);
+    if (ntiles > 1) {
+      dma_tile<BM, AK>(rsA, g.lda, kA0 + BK, smem + C::STAGE_BYTES, wave, lane);
+      dma_tile<BN, BKM>(rsB, g.ldb, kB0 + BK, smem + C::STAGE_BYTES + C::A_BYTES, wave, lane);
+      __builtin_amdgcn_s_waitcnt(WAIT_ONE_TILE_IN_FLIGHT);
+    } else {
+      __builtin_amdgcn_s_waitcnt(WAIT_ALL);
     }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < TM; ++i) af[0][i] = frag<BM, AK>(smem, wm * C::WM + i * 32, 0, lane);
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+      bfr[0][j] = frag<BN, BKM>(smem + C::A_BYTES, wn * C::WN + j * 32, 0, lane);
+  }
+  // Main loop.  While the MFMAs of k-step ks run, the fragments of ks + 1 are
+  // read; in the last k-step of a tile the fragments come from the next tile
+  // instead: wait for this wavefront's loads of tile t + 1 and its reads of
+  // tile t, barrier (every wavefront's tile t + 1 has landed and nobody reads
+  // tile t's buffer any more), refill that buffer with tile t + 2, then read.
+  for (int t = 0; t < ntiles; ++t) {
     const char* As = smem + (t & 1) * C::STAGE_BYTES;
     const char* Bs = As + C::A_BYTES;
-    // Fragments of k-step ks + 1 are read while the MFMAs of ks run.
-    bf16x8_t af[2][TM], bfr[2][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i) af[0][i] = frag<BM, AK>(As, wm * C::WM + i * 32, 0, lane);
-#pragma unroll
-    for (int j = 0; j < TN; ++j) bfr[0][j] = frag<BN, BKM>(Bs, wn * C::WN + j * 32, 0, lane);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const int cur = ks & 1, nxt = cur ^ 1;
@@ -289,9 +303,23 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
         for (int i = 0; i < TM; ++i) af[nxt][i] = frag<BM, AK>(As, wm * C::WM + i * 32, ks + 1, lane);
 #pragma unroll
         for (int j = 0; j < TN; ++j) bfr[nxt][j] = frag<BN, BKM>(Bs, wn * C::WN + j * 32, ks + 1, lane);
+      } else if (t + 1 < ntiles) {
+        __builtin_amdgcn_s_waitcnt(WAIT_ALL);
+        __syncthreads();
+        if (t + 2 < ntiles) {
+          char* nb = smem + (t & 1) * C::STAGE_BYTES;
+          dma_tile<BM, AK>(rsA, g.lda, kA0 + (t + 2) * BK, nb, wave, lane);
+          dma_tile<BN, BKM>(rsB, g.ldb, kB0 + (t + 2) * BK, nb + C::A_BYTES, wave, lane);
+        }
+        const char* An = smem + ((t + 1) & 1) * C::STAGE_BYTES;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) af[nxt][i] = frag<BM, AK>(An, wm * C::WM + i * 32, 0, lane);
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          bfr[nxt][j] = frag<BN, BKM>(An + C::A_BYTES, wn * C::WN + j * 32, 0, lane);
       }
-      // Keep the scheduler from sinking the fragment reads of ks + 1 down to
-      // their uses: they must be in flight while these MFMAs execute.
+      // Keep the scheduler from sinking the fragment reads down to their
+      // uses: they must be in flight while these MFMAs execute.
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
