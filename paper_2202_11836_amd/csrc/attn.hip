@@ -151,7 +151,7 @@ __global__ __launch_bounds__(256) void key_extent_kernel(const uint8_t* __restri
 // ---------------------------------------------------------------------------
 // Forward: wavefront = 32 queries; block = 128 queries of one (batch, head).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void attn_fwd_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t Ks[KT * LD];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[HD * LDT];
   __shared__ uint8_t ms[KT];
@@ -237,7 +237,7 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(AttnArgs a) {
 // ---------------------------------------------------------------------------
 // Backward, dQ: wavefront = 32 queries; loops over key blocks.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t Ks[KT * LD];
   __shared__ __attribute__((aligned(16))) bf16_t Kt[HD * LDT];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[KT * LD];
@@ -317,7 +317,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnArgs a) {
 // ---------------------------------------------------------------------------
 // Backward, dK and dV: wavefront = 32 keys; loops over query blocks.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t Qs[KT * LD];
   __shared__ __attribute__((aligned(16))) bf16_t Qt[HD * LDT];
   __shared__ __attribute__((aligned(16))) bf16_t dOs[KT * LD];
