@@ -105,10 +105,11 @@ __device__ __forceinline__ void load_rows_t(const bf16_t* __restrict__ src, int6
 // Write a wavefront's 32 x 64 result, held transposed in two accumulators
 // (lane = row l % 32, registers = columns), to dst rows [row0, row0 + 32)
 // clipped to nrows: staged through the wavefront's LDS area (32 x LD) so
-// that the global stores are 16-byte row segments.
+// that the global stores are 16-byte row segments.  If colsum is not null it
+// receives the 64 column sums of the stored (bf16) values of those rows.
 __device__ __forceinline__ void store_rows_t(const f32x16_t acc[2], float mul, bf16_t* stage,
                                              bf16_t* __restrict__ dst, int64_t ld, int row0,
-                                             int nrows) {
+                                             int nrows, float* colsum) {
   const int lane = threadIdx.x & 63, hf = lane >> 5, rr = lane & 31;
 #pragma unroll
   for (int t = 0; t < 2; ++t)
@@ -124,12 +125,34 @@ __device__ __forceinline__ void store_rows_t(const f32x16_t acc[2], float mul, b
     }
   __builtin_amdgcn_s_waitcnt(0);
   __builtin_amdgcn_wave_barrier();
+  // lane owns column chunk (lane & 7) * 8 and rows (lane >> 3) + 8 i
+  float cs[8] = {0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     int c = lane + 64 * i;
     int row = c >> 3, c8 = (c & 7) * 8;
-    if (row0 + row < nrows)
-      *(u32x4_t*)(dst + (int64_t)(row0 + row) * ld + c8) = *(const u32x4_t*)(stage + row * LD + c8);
+    if (row0 + row < nrows) {
+      const u32x4_t v = *(const u32x4_t*)(stage + row * LD + c8);
+      *(u32x4_t*)(dst + (int64_t)(row0 + row) * ld + c8) = v;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        cs[2 * e] += __uint_as_float(v[e] << 16);
+        cs[2 * e + 1] += __uint_as_float(v[e] & 0xffff0000u);
+      }
+    }
+  }
+  if (colsum) {
+    // lanes with equal lane & 7 hold the same columns: fixed-order sum
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      cs[e] += __shfl_xor(cs[e], 8, 64);
+      cs[e] += __shfl_xor(cs[e], 16, 64);
+      cs[e] += __shfl_xor(cs[e], 32, 64);
+    }
+    if (lane < 8) {
+      *(f32x4_t*)(colsum + lane * 8) = f32x4_t{cs[0], cs[1], cs[2], cs[3]};
+      *(f32x4_t*)(colsum + lane * 8 + 4) = f32x4_t{cs[4], cs[5], cs[6], cs[7]};
+    }
   }
 }
 
@@ -231,7 +254,7 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
   const float inv = ltot > 0.0f ? 1.0f / ltot : 0.0f;
   if (hf == 0 && q0 + rr < S)
     a.lse[(int64_t)bh * S + q0 + rr] = ltot > 0.0f ? m + __log2f(ltot) : 0.0f;
-  store_rows_t(acc, inv, stage[wave], a.out + (int64_t)b * S * h + j * HD, h, q0, S);
+  store_rows_t(acc, inv, stage[wave], a.out + (int64_t)b * S * h + j * HD, h, q0, S, nullptr);
 }
 
 // ---------------------------------------------------------------------------
@@ -311,7 +334,9 @@ __global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
       }
     }
   }
-  store_rows_t(dq, a.scale, stage[wave], a.out + (int64_t)b * S * ld + j * HD, ld, q0, S);
+  const int nqb = (S + 31) / 32;
+  float* cp = (a.colpart && q0 < S) ? a.colpart + ((int64_t)b * nqb + q0 / 32) * ld + j * HD : nullptr;
+  store_rows_t(dq, a.scale, stage[wave], a.out + (int64_t)b * S * ld + j * HD, ld, q0, S, cp);
 }
 
 // ---------------------------------------------------------------------------
@@ -397,9 +422,11 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
   // Stage the outputs through the (now free) Q tiles: 4 waves x 32 x LD.
   bf16_t* stage = (wave < 2 ? Qs : dOs) + (wave & 1) * 32 * LD;
   bf16_t* dst = a.out + (int64_t)b * S * ld + j * HD;
-  store_rows_t(dk, a.scale, stage, dst + h, ld, k0, S);
+  const int nqb = (S + 31) / 32;
+  float* cp = (a.colpart && k0 < S) ? a.colpart + ((int64_t)b * nqb + k0 / 32) * ld + j * HD : nullptr;
+  store_rows_t(dk, a.scale, stage, dst + h, ld, k0, S, cp ? cp + h : nullptr);
   __builtin_amdgcn_wave_barrier();
-  store_rows_t(dv, 1.0f, stage, dst + 2 * h, ld, k0, S);
+  store_rows_t(dv, 1.0f, stage, dst + 2 * h, ld, k0, S, cp ? cp + 2 * h : nullptr);
 }
 
 }  // namespace

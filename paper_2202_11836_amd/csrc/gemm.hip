@@ -148,6 +148,7 @@ __device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
 }
 
 // Epilogue for 8 consecutive columns n..n+7 of row m (n % 8 == 0, n < N).
+// For EPI_DGELU, v returns the values as stored.
 template <int EPI, bool OUTF32>
 __device__ __forceinline__ void epi8(const GemmArgs& g, int64_t offC, int zs, int m, int n,
                                      float v[8]) {
@@ -196,6 +197,13 @@ __device__ __forceinline__ void epi8(const GemmArgs& g, int64_t offC, int zs, in
 #pragma unroll
   for (int i = 0; i < 4; ++i) o[i] = pack_bf2(v[2 * i], v[2 * i + 1]);
   *(u32x4_t*)((bf16_t*)g.C + offC + idx) = o;
+  if (EPI == EPI_DGELU) {  // hand back the stored (rounded) values
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(o[i] << 16);
+      v[2 * i + 1] = __uint_as_float(o[i] & 0xffff0000u);
+    }
+  }
   if (EPI == EPI_GELU) {
     // GELU of the stored (rounded) U, so that forward and backward agree.
     u32x4_t q;
@@ -338,6 +346,10 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
   float* stg = (float*)smem + wave * 32 * C::EPI_LD;
   const int mw = m0 + wm * C::WM, nw = n0 + wn * C::WN;
   constexpr int CH = C::WN / 8;  // 8-column chunks per staged row
+  // Optional column sums (EPI_DGELU): every lane keeps one 8-column chunk
+  // (CH divides 64) over the rows it writes.
+  constexpr bool COLSUM = EPI == EPI_DGELU && CH == 16 && C::WM == 128;
+  float csum[8] = {0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -359,9 +371,29 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
         v[e] = x0[e];
         v[4 + e] = x1[e];
       }
-      if (m < g.M && n < g.N) epi8<EPI, OUTF32>(g, offC, zs, m, n, v);
+      if (m < g.M && n < g.N) {
+        epi8<EPI, OUTF32>(g, offC, zs, m, n, v);
+        if (COLSUM) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) csum[e] += v[e];
+        }
+      }
     }
     __builtin_amdgcn_wave_barrier();
+  }
+  if (COLSUM && g.colpart) {
+    // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same columns: fixed-order sum
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      csum[e] += __shfl_xor(csum[e], 16, 64);
+      csum[e] += __shfl_xor(csum[e], 32, 64);
+    }
+    const int n = nw + (lane & 15) * 8;
+    if (lane < 16 && n < g.N) {
+      float* P = g.colpart + (int64_t)(mw / C::WM) * g.N + n;
+      *(f32x4_t*)P = f32x4_t{csum[0], csum[1], csum[2], csum[3]};
+      *(f32x4_t*)(P + 4) = f32x4_t{csum[4], csum[5], csum[6], csum[7]};
+    }
   }
 }
 

@@ -39,6 +39,9 @@ struct GemmArgs {
   int kchunk;
   float alpha;
   int tile;  // bf16 tile shape: 0 = automatic, 1 = 256x256, 2 = 256x128, 3 = 128x128
+  // EPI_DGELU on bf16, optional: column sums of the stored output per block
+  // of 128 rows, colpart[m / 128][n] (needs tile 1).
+  float* colpart;
 };
 
 inline GemmArgs gemm_args(const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
@@ -112,6 +115,9 @@ hipError_t softmax_bwd(const float* dP, const T* P, T* dS, int BH, int S, int ld
 //   dsum: [B*H, S] fp32 rowsum(dO * O) (written by attn_backward_dq)
 // ---------------------------------------------------------------------------
 struct AttnArgs {
+  // backward, optional: column sums of dQKV per 32-row block of each
+  // sequence, colpart[b * ceil(S / 32) + s / 32][3h]
+  float* colpart;
   const bf16_t* qkv;
   const uint8_t* mask;
   const int* kext;

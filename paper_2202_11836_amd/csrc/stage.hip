@@ -118,7 +118,7 @@ struct stage {
   std::vector<void*> allocs;  // parameter / gradient memory
 
   // Activation memory, sized for cap_T tokens and cap_BSS score entries.
-  int64_t cap_T = -1, cap_BSS = -1, cap_B = -1;
+  int64_t cap_T = -1, cap_BSS = -1, cap_B = -1, cap_NQB = -1;
   std::vector<void*> act_allocs;
   std::vector<Saved> saved;
   uint8_t* mask = nullptr;
@@ -136,6 +136,8 @@ struct stage {
   void* dC = nullptr;       // [T, h]
   void* dY = nullptr;       // [T, h] gradient flowing between layers
   float* part = nullptr;    // column-sum partials
+  float* colpart_ffn = nullptr;  // [ceil(T/128), f] column sums of dU (bf16 stages)
+  float* colpart_qkv = nullptr;  // [B * ceil(S/32), 3h] column sums of dQKV (bf16 stages)
   // Transposed weights of the layer being differentiated (bf16 stages), so
   // that every data-gradient GEMM reads both operands k-contiguously.
   void* wt_qkv = nullptr;   // [h, 3h]
@@ -225,7 +227,7 @@ void free_activations(stage_t* s) {
   for (void* p : s->act_allocs) (void)hipFree(p);
   s->act_allocs.clear();
   s->saved.clear();
-  s->cap_T = s->cap_BSS = s->cap_B = -1;
+  s->cap_T = s->cap_BSS = s->cap_B = s->cap_NQB = -1;
   s->have_ctx = false;
 }
 
@@ -268,7 +270,9 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
   // The score matrix is materialised only on fp32 stages.
   const int64_t BSS = s->dtype == STAGE_F32 ? (int64_t)B * s->H * S * S : 0;
   const int64_t BHS = (int64_t)B * s->H * S;
-  if (T <= s->cap_T && BSS <= s->cap_BSS && B <= s->cap_B && (int)s->saved.size() == s->L)
+  const int64_t NQB = (int64_t)B * ((S + 31) / 32);
+  if (T <= s->cap_T && BSS <= s->cap_BSS && B <= s->cap_B && NQB <= s->cap_NQB &&
+      (int)s->saved.size() == s->L)
     return STAGE_OK;
   free_activations(s);
   const size_t e = s->esz;
@@ -293,6 +297,10 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
       (st = A(&s->dU, T * f * e)) || (st = A(&s->dH1, T * h * e)) ||
       (st = A(&s->dZ1, T * h * e)) || (st = A(&s->dC, T * h * e)) || (st = A(&s->dY, T * h * e)))
     return st;
+  const int64_t nqb = ((int64_t)S + 31) / 32;
+  if ((st = A((void**)&s->colpart_ffn, ((T + 127) / 128) * f * 4)) ||
+      (st = A((void**)&s->colpart_qkv, (int64_t)B * nqb * 3 * h * 4)))
+    return st;
   if ((st = A(&s->wt_qkv, 3 * h * h * e)) || (st = A(&s->wt_o, h * h * e)) ||
       (st = A(&s->wt_1, f * h * e)) || (st = A(&s->wt_2, h * f * e)))
     return st;
@@ -313,6 +321,7 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
   s->cap_T = T;
   s->cap_BSS = BSS;
   s->cap_B = B;
+  s->cap_NQB = NQB;
   return STAGE_OK;
 }
 
@@ -525,9 +534,18 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
       GemmArgs g = gemm_args(dZ2, h, W2, kBF ? h : f, dU, f, Tn, f, h);
       g.aux = v.U;
       g.ldaux = f;
+      if (kBF) {  // db_1 = column sums of dU, accumulated in the epilogue
+        g.tile = 1;
+        g.colpart = s->colpart_ffn;
+      }
       SITE(FFN2_DGRAD, Gemm<T>::run(g, true, kBF, EPI_DGELU, false, 1, st));
     }
-    if ((r = col_sum<T>(s, SITE_B1_SUM, SITE_B1_RED, dU, f, gr[STAGE_B_1]))) return r;
+    if (kBF) {
+      float* outs[1] = {gr[STAGE_B_1]};
+      SITE(B1_RED, col_reduce(s->colpart_ffn, (Tn + 127) / 128, 1, f, outs, st));
+    } else if ((r = col_sum<T>(s, SITE_B1_SUM, SITE_B1_RED, dU, f, gr[STAGE_B_1]))) {
+      return r;
+    }
     // dW_1 = dU^T H1
     if ((r = wgrad<T>(s, SITE_W1_WGRAD, SITE_W1_RED, dU, f, (const T*)v.H1, h, f, h, Tn, gr[STAGE_W_1]))) return r;
     // dH1 = dZ2 + dU W_1
@@ -552,8 +570,11 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
       AttnArgs aa = attn_args(s, (const bf16_t*)QKV, (bf16_t*)dQKV, v.lse);
       aa.o = (const bf16_t*)v.C;
       aa.dout = (const bf16_t*)dC;
+      aa.colpart = s->colpart_qkv;  // db_qkv: column sums per 32-row block
       SITE(ATTN_DQ, attn_backward_dq(aa, st));
       SITE(ATTN_DKDV, attn_backward_dkdv(aa, st));
+      float* outs[1] = {gr[STAGE_B_QKV]};
+      SITE(BQKV_RED, col_reduce(s->colpart_qkv, B * ((S + 31) / 32), 1, 3 * h, outs, st));
     } else {
     // dP[b, j] = dC_bj V_bj^T (fp32, into the score buffer)
     {
@@ -606,7 +627,8 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
       SITE(DK_BWD, Gemm<T>::run(g, false, false, EPI_STORE, false, BH, st));
     }
     }
-    if ((r = col_sum<T>(s, SITE_BQKV_SUM, SITE_BQKV_RED, dQKV, 3 * h, gr[STAGE_B_QKV]))) return r;
+    if (!kBF && (r = col_sum<T>(s, SITE_BQKV_SUM, SITE_BQKV_RED, dQKV, 3 * h, gr[STAGE_B_QKV])))
+      return r;
     // dW_qkv = dQKV^T X
     if ((r = wgrad<T>(s, SITE_WQKV_WGRAD, SITE_WQKV_RED, dQKV, 3 * h, (const T*)v.X, h, 3 * h, h, Tn, gr[STAGE_W_QKV]))) return r;
     // dX = dZ1 + dQKV W_qkv  (the previous layer's dY, or the stage's dx)
