@@ -73,7 +73,7 @@ typedef enum {
   STAGE_SAVED_QKV = 1, /* Q | K | V             [T, 3h] dtype */
   STAGE_SAVED_CTX = 2, /* attention context     [T, h]  dtype */
   STAGE_SAVED_H1 = 3,  /* first LayerNorm out   [T, h]  dtype */
-  STAGE_SAVED_U = 4,   /* FFN pre-activation    [T, f]  dtype */
+  STAGE_SAVED_GD = 4,  /* GELU'(U), U = FFN pre-activation [T, f] dtype */
   STAGE_SAVED_G = 5,   /* GELU(U)               [T, f]  dtype */
   STAGE_NSAVED = 6
 } stage_saved_id;

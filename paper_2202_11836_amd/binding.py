@@ -18,7 +18,7 @@ STAGE_OK, STAGE_EINVAL, STAGE_ESTATE, STAGE_ENOMEM, STAGE_EHIP = range(5)
 STAGE_F32, STAGE_BF16 = 0, 1
 PARAM_NAMES = ("W_qkv", "b_qkv", "W_o", "b_o", "g1", "be1",
                "W_1", "b_1", "W_2", "b_2", "g2", "be2")
-SAVED_NAMES = ("X", "QKV", "CTX", "H1", "U", "G")
+SAVED_NAMES = ("X", "QKV", "CTX", "H1", "GD", "G")  # GD = GELU'(U)
 KIND_PARAM, KIND_GRAD, KIND_SAVED = 0, 1, 2
 STATUS_NAMES = {0: "OK", 1: "EINVAL", 2: "ESTATE", 3: "ENOMEM", 4: "EHIP"}
 

@@ -148,7 +148,7 @@ __device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
 }
 
 // Epilogue for 8 consecutive columns n..n+7 of row m (n % 8 == 0, n < N).
-// For EPI_DGELU, v returns the values as stored.
+// For EPI_MUL, v returns the values as stored.
 template <int EPI, bool OUTF32>
 __device__ __forceinline__ void epi8(const GemmArgs& g, int64_t offC, int zs, int m, int n,
                                      float v[8]) {
@@ -179,41 +179,52 @@ __device__ __forceinline__ void epi8(const GemmArgs& g, int64_t offC, int zs, in
     *(f32x4_t*)(C + 4) = f32x4_t{v[4], v[5], v[6], v[7]};
     return;
   }
-  if (EPI == EPI_DGELU || EPI == EPI_RESID) {
+  if (EPI == EPI_MUL || EPI == EPI_RESID) {
     const u32x4_t x = *(const u32x4_t*)((const bf16_t*)g.aux + offC + (int64_t)m * g.ldaux + n);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const float a0 = __uint_as_float(x[i] << 16), a1 = __uint_as_float(x[i] & 0xffff0000u);
-      if (EPI == EPI_DGELU) {
-        v[2 * i] *= gelu_grad_f(a0);
-        v[2 * i + 1] *= gelu_grad_f(a1);
+      if (EPI == EPI_MUL) {
+        v[2 * i] *= a0;
+        v[2 * i + 1] *= a1;
       } else {
         v[2 * i] += a0;
         v[2 * i + 1] += a1;
       }
     }
   }
+  if (EPI == EPI_GELU) {
+    // v holds u = acc + bias: store GELU(u) and GELU'(u)
+    u32x4_t o, q;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float gv[2], dv[2];
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const float u = v[2 * i + e];
+        const ErfParts p = erf_parts(u);
+        gv[e] = 0.5f * u * p.onep;
+        dv[e] = fmaf(u * 0.39894228040143268f, p.e, 0.5f * p.onep);
+      }
+      o[i] = pack_bf2(gv[0], gv[1]);
+      q[i] = pack_bf2(dv[0], dv[1]);
+    }
+    *(u32x4_t*)((bf16_t*)g.C + offC + idx) = o;
+    *(u32x4_t*)((bf16_t*)g.C2 + offC + idx) = q;
+    return;
+  }
   u32x4_t o;
 #pragma unroll
   for (int i = 0; i < 4; ++i) o[i] = pack_bf2(v[2 * i], v[2 * i + 1]);
   *(u32x4_t*)((bf16_t*)g.C + offC + idx) = o;
-  if (EPI == EPI_DGELU) {  // hand back the stored (rounded) values
+  if (EPI == EPI_MUL) {  // hand back the stored (rounded) values
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       v[2 * i] = __uint_as_float(o[i] << 16);
       v[2 * i + 1] = __uint_as_float(o[i] & 0xffff0000u);
     }
   }
-  if (EPI == EPI_GELU) {
-    // GELU of the stored (rounded) U, so that forward and backward agree.
-    u32x4_t q;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float u0 = __uint_as_float(o[i] << 16), u1 = __uint_as_float(o[i] & 0xffff0000u);
-      q[i] = pack_bf2(gelu_f(u0), gelu_f(u1));
-    }
-    *(u32x4_t*)((bf16_t*)g.C2 + offC + idx) = q;
-  }
+
 }
 
 template <int BM, int BN, bool AK, bool BKM, int EPI, bool OUTF32>
@@ -346,9 +357,9 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
   float* stg = (float*)smem + wave * 32 * C::EPI_LD;
   const int mw = m0 + wm * C::WM, nw = n0 + wn * C::WN;
   constexpr int CH = C::WN / 8;  // 8-column chunks per staged row
-  // Optional column sums (EPI_DGELU): every lane keeps one 8-column chunk
+  // Optional column sums (EPI_MUL): every lane keeps one 8-column chunk
   // (CH divides 64) over the rows it writes.
-  constexpr bool COLSUM = EPI == EPI_DGELU && CH == 16 && C::WM == 128;
+  constexpr bool COLSUM = EPI == EPI_MUL && CH == 16 && C::WM == 128;
   float csum[8] = {0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
@@ -410,12 +421,12 @@ __device__ __forceinline__ void epi_store_f32(const GemmArgs& g, int64_t offC, i
     if (g.bias) v += g.bias[n];
     ((float*)g.C + offC)[(int64_t)m * g.ldc + n] = v;
   } else if (EPI == EPI_GELU) {
-    float u = v + g.bias[n];
-    ((float*)g.C + offC)[(int64_t)m * g.ldc + n] = u;
-    ((float*)g.C2 + offC)[(int64_t)m * g.ldc + n] = gelu_f(u);
-  } else if (EPI == EPI_DGELU) {
-    float u = ((const float*)g.aux + offC)[(int64_t)m * g.ldaux + n];
-    ((float*)g.C + offC)[(int64_t)m * g.ldc + n] = v * gelu_grad_f(u);
+    const float u = v + g.bias[n];
+    ((float*)g.C + offC)[(int64_t)m * g.ldc + n] = gelu_f(u);
+    ((float*)g.C2 + offC)[(int64_t)m * g.ldc + n] = gelu_grad_f(u);
+  } else if (EPI == EPI_MUL) {
+    const float d = ((const float*)g.aux + offC)[(int64_t)m * g.ldaux + n];
+    ((float*)g.C + offC)[(int64_t)m * g.ldc + n] = v * d;
   } else if (EPI == EPI_RESID) {
     float r = ((const float*)g.aux + offC)[(int64_t)m * g.ldaux + n];
     ((float*)g.C + offC)[(int64_t)m * g.ldc + n] = v + r;
@@ -507,7 +518,7 @@ hipError_t dispatch_epi(const GemmArgs& g, GemmEpi epi, bool out_f32, int batch,
       return out_f32 ? launch_bf16<BM, BN, AK, BKM, EPI_STORE, true>(g, batch, st)
                      : launch_bf16<BM, BN, AK, BKM, EPI_STORE, false>(g, batch, st);
     case EPI_GELU: return launch_bf16<BM, BN, AK, BKM, EPI_GELU, false>(g, batch, st);
-    case EPI_DGELU: return launch_bf16<BM, BN, AK, BKM, EPI_DGELU, false>(g, batch, st);
+    case EPI_MUL: return launch_bf16<BM, BN, AK, BKM, EPI_MUL, false>(g, batch, st);
     case EPI_RESID: return launch_bf16<BM, BN, AK, BKM, EPI_RESID, false>(g, batch, st);
     case EPI_PARTIAL: return launch_bf16<BM, BN, AK, BKM, EPI_PARTIAL, true>(g, batch, st);
   }
@@ -532,8 +543,8 @@ hipError_t dispatch_f32(const GemmArgs& g, GemmEpi epi, int batch, hipStream_t s
       hipLaunchKernelGGL((gemm_f32_kernel<AK, BKM, EPI_STORE>), grid, dim3(NT), 0, st, g); break;
     case EPI_GELU:
       hipLaunchKernelGGL((gemm_f32_kernel<AK, BKM, EPI_GELU>), grid, dim3(NT), 0, st, g); break;
-    case EPI_DGELU:
-      hipLaunchKernelGGL((gemm_f32_kernel<AK, BKM, EPI_DGELU>), grid, dim3(NT), 0, st, g); break;
+    case EPI_MUL:
+      hipLaunchKernelGGL((gemm_f32_kernel<AK, BKM, EPI_MUL>), grid, dim3(NT), 0, st, g); break;
     case EPI_RESID:
       hipLaunchKernelGGL((gemm_f32_kernel<AK, BKM, EPI_RESID>), grid, dim3(NT), 0, st, g); break;
     case EPI_PARTIAL:

@@ -18,8 +18,8 @@
 // ---------------------------------------------------------------------------
 enum GemmEpi {
   EPI_STORE = 0,    // C = alpha * acc (+ bias[n] when bias != nullptr)
-  EPI_GELU = 1,     // U = acc + bias[n] -> C;  GELU(U) -> C2
-  EPI_DGELU = 2,    // C = acc * GELU'(aux[m, n])
+  EPI_GELU = 1,     // u = acc + bias[n]:  GELU(u) -> C;  GELU'(u) -> C2
+  EPI_MUL = 2,      // C = acc * aux[m, n]  (the FFN backward: dU = dG * GELU'(u))
   EPI_RESID = 3,    // C = acc + aux[m, n]
   EPI_PARTIAL = 4,  // fp32 C[split][m][n] = acc over this split's K range
 };
@@ -39,7 +39,7 @@ struct GemmArgs {
   int kchunk;
   float alpha;
   int tile;  // bf16 tile shape: 0 = automatic, 1 = 256x256, 2 = 256x128, 3 = 128x128
-  // EPI_DGELU on bf16, optional: column sums of the stored output per block
+  // EPI_MUL on bf16, optional: column sums of the stored output per block
   // of 128 rows, colpart[m / 128][n] (needs tile 1).
   float* colpart;
 };

@@ -100,7 +100,7 @@ struct Saved {
   void* xhat1 = nullptr; // [T, h]
   float* rstd1 = nullptr;
   void* H1 = nullptr;    // [T, h]
-  void* U = nullptr;     // [T, f]
+  void* Gd = nullptr;    // GELU'(U) [T, f], U = H1 W_1^T + b_1
   void* G = nullptr;     // [T, f]
   void* xhat2 = nullptr; // [T, h]
   float* rstd2 = nullptr;
@@ -285,7 +285,7 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
     if ((st = A(&v.X, T * h * e)) || (st = A(&v.QKV, T * 3 * h * e)) ||
         (st = A(&v.P, BSS * e)) || (st = A((void**)&v.lse, BHS * 4)) || (st = A(&v.C, T * h * e)) || (st = A(&v.xhat1, T * h * e)) ||
         (st = A((void**)&v.rstd1, T * 4)) || (st = A(&v.H1, T * h * e)) ||
-        (st = A(&v.U, T * f * e)) || (st = A(&v.G, T * f * e)) ||
+        (st = A(&v.Gd, T * f * e)) || (st = A(&v.G, T * f * e)) ||
         (st = A(&v.xhat2, T * h * e)) || (st = A((void**)&v.rstd2, T * 4)))
       return st;
   }
@@ -441,11 +441,11 @@ stage_status forward_impl(stage_t* s, const T* x, T* y) {
     SITE(LN1_FWD, add_ln_fwd<T, float, T>(s->tmp, (const float*)p[STAGE_B_O], X,
                                    (const float*)p[STAGE_G1], (const float*)p[STAGE_BE1],
                                    (T*)v.H1, h1_32, (T*)v.xhat1, v.rstd1, Tn, h, st));
-    // U = H1 W_1^T + b_1;  G = GELU(U)
+    // U = H1 W_1^T + b_1;  G = GELU(U) and GELU'(U) (kept for the backward)
     {
-      GemmArgs g = gemm_args(v.H1, h, p[STAGE_W_1], h, v.U, f, Tn, f, h);
+      GemmArgs g = gemm_args(v.H1, h, p[STAGE_W_1], h, v.G, f, Tn, f, h);
       g.bias = (const float*)p[STAGE_B_1];
-      g.C2 = v.G;
+      g.C2 = v.Gd;
       SITE(FFN1_FWD, Gemm<T>::run(g, true, true, EPI_GELU, false, 1, st));
     }
     // tmp = G W_2^T (fp32);  Y = LN(H1 + tmp + b_2)
@@ -532,13 +532,13 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
     // dU = (dZ2 W_2) * GELU'(U)
     {
       GemmArgs g = gemm_args(dZ2, h, W2, kBF ? h : f, dU, f, Tn, f, h);
-      g.aux = v.U;
+      g.aux = v.Gd;
       g.ldaux = f;
       if (kBF) {  // db_1 = column sums of dU, accumulated in the epilogue
         g.tile = 1;
         g.colpart = s->colpart_ffn;
       }
-      SITE(FFN2_DGRAD, Gemm<T>::run(g, true, kBF, EPI_DGELU, false, 1, st));
+      SITE(FFN2_DGRAD, Gemm<T>::run(g, true, kBF, EPI_MUL, false, 1, st));
     }
     if (kBF) {
       float* outs[1] = {gr[STAGE_B_1]};
@@ -825,7 +825,7 @@ static void* saved_ptr(stage_t* s, int layer, int which, size_t* bytes) {
     case STAGE_SAVED_QKV: *bytes = T * 3 * s->h * e; return v.QKV;
     case STAGE_SAVED_CTX: *bytes = T * s->h * e; return v.C;
     case STAGE_SAVED_H1: *bytes = T * s->h * e; return v.H1;
-    case STAGE_SAVED_U: *bytes = T * s->f * e; return v.U;
+    case STAGE_SAVED_GD: *bytes = T * s->f * e; return v.Gd;
     case STAGE_SAVED_G: *bytes = T * s->f * e; return v.G;
   }
   *bytes = 0;

@@ -49,12 +49,15 @@ def check_f32(cfg, got, ref, saved_gpu=None):
             assert e <= F32_TOL, (l, name, e)
     if saved_gpu:
         from oracle import merge_heads
-        for which, key in ((1, "QKV"), (2, "C"), (3, "H1"), (4, "U"), (5, "G")):
+        from oracle import gelu_grad
+        for which, key in ((1, "QKV"), (2, "C"), (3, "H1"), (4, "GD"), (5, "G")):
             for l in range(cfg.L):
                 sv = ref["saved"][l]
                 if key == "QKV":
                     r = np.concatenate([merge_heads(sv["Q"]), merge_heads(sv["K"]),
                                         merge_heads(sv["V"])], axis=1)
+                elif key == "GD":
+                    r = gelu_grad(sv["U"])
                 else:
                     r = sv[key]
                 e = rel_inf(saved_gpu[which][l], r)
