@@ -9,6 +9,7 @@
 // k-tile overlaps the MFMAs of the last k-step.  Operands stored m/n-contiguous in
 // HBM keep that layout in LDS and their MFMA fragments are read with gfx950's
 // transposing LDS read.
+#include <algorithm>
 #include <type_traits>
 
 #include "kernels.h"
@@ -39,6 +40,26 @@ __device__ __forceinline__ void tile_of_block(int nbm, int nbn, int& tm, int& tn
   tn = r / gsize;
 }
 
+// Linear tile index -> (z, m tile, n tile) for a persistent grid.  Work-group
+// w starts on XCD w % 8 and keeps it (the grid is a multiple of 8), so the
+// tile ranges are dealt out per XCD as above.
+__device__ __forceinline__ void decode_tile(int vt, int total, int nbm, int nbn, int& z, int& tm,
+                                            int& tn) {
+  int bid = vt;
+  if ((total & 7) == 0) bid = (vt & 7) * (total >> 3) + (vt >> 3);
+  const int per_z = nbm * nbn;
+  z = bid / per_z;
+  const int r0 = bid - z * per_z;
+  constexpr int GM = 8;
+  const int per_group = GM * nbn;
+  const int group = r0 / per_group;
+  const int first_m = group * GM;
+  const int gsize = min(nbm - first_m, GM);
+  const int r = r0 - group * per_group;
+  tm = first_m + r % gsize;
+  tn = r / gsize;
+}
+
 __device__ __forceinline__ int64_t batch_off(int zb, int zdiv, int64_t s1, int64_t s2) {
   return (int64_t)(zb / zdiv) * s1 + (int64_t)(zb % zdiv) * s2;
 }
@@ -62,10 +83,9 @@ struct TileCfg {
   static constexpr int TM = WM / 32, TN = WN / 32;
   static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
   static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
-  static constexpr int EPI_LD = WN + 4;  // fp32 staging row
-  static constexpr int LDS_BYTES_MAIN = 2 * STAGE_BYTES;
-  static constexpr int LDS_BYTES_EPI = 4 * 32 * EPI_LD * 4;
-  static constexpr int LDS_BYTES = LDS_BYTES_MAIN > LDS_BYTES_EPI ? LDS_BYTES_MAIN : LDS_BYTES_EPI;
+  // Epilogue staging, beside the two stages: 16 rows x WN fp32 per wavefront.
+  static constexpr int EPI_BYTES = 4 * 16 * WN * 4;
+  static constexpr int LDS_BYTES = 2 * STAGE_BYTES + EPI_BYTES;
 };
 
 // Buffer resource over [base, base + bytes): loads past the end return 0.
@@ -227,6 +247,53 @@ __device__ __forceinline__ void epi8(const GemmArgs& g, int64_t offC, int zs, in
 
 }
 
+// One output tile's operands: buffer resources and k-tile range.
+struct TileOps {
+  __amdgpu_buffer_rsrc_t rsA, rsB;
+  int kA0, kB0;     // first k of the range, relative to each resource
+  int ntiles;       // k-tiles
+  int m0, n0, zs, zb;
+};
+
+template <int BM, int BN, bool AK, bool BKM>
+__device__ __forceinline__ TileOps tile_ops(const GemmArgs& g, int vt, int total, int nbm, int nbn) {
+  TileOps o;
+  int z, tm, tn;
+  decode_tile(vt, total, nbm, nbn, z, tm, tn);
+  o.zs = z % g.ksplit;
+  o.zb = z / g.ksplit;
+  o.m0 = tm * BM;
+  o.n0 = tn * BN;
+  const bf16_t* A = (const bf16_t*)g.A + batch_off(o.zb, g.zdiv, g.sA1, g.sA2);
+  const bf16_t* B = (const bf16_t*)g.B + batch_off(o.zb, g.zdiv, g.sB1, g.sB2);
+  const int kbeg = o.zs * g.kchunk;
+  const int kend = min(g.K, kbeg + g.kchunk);
+  o.ntiles = (kend - kbeg + 63) / 64;
+  // k-major: from the tile's first row to the operand's last row (rows past
+  // it read 0; K is a multiple of 64).  m/n-major: from this split's first
+  // k-row and the tile's first column to the end of the operand (k-rows past
+  // K read 0; reads past the valid columns of a row only feed output rows /
+  // columns that are never stored).
+  if constexpr (AK) {
+    o.rsA = make_rsrc(A + (int64_t)o.m0 * g.lda, (int64_t)(g.M - o.m0) * g.lda * 2);
+    o.kA0 = kbeg;
+  } else {
+    o.rsA = make_rsrc(A + (int64_t)kbeg * g.lda + o.m0, ((int64_t)(g.K - kbeg) * g.lda - o.m0) * 2);
+    o.kA0 = 0;
+  }
+  if constexpr (BKM) {
+    o.rsB = make_rsrc(B + (int64_t)o.n0 * g.ldb, (int64_t)(g.N - o.n0) * g.ldb * 2);
+    o.kB0 = kbeg;
+  } else {
+    o.rsB = make_rsrc(B + (int64_t)kbeg * g.ldb + o.n0, ((int64_t)(g.K - kbeg) * g.ldb - o.n0) * 2);
+    o.kB0 = 0;
+  }
+  return o;
+}
+
+// Persistent kernel: each work-group walks output tiles vt = blockIdx.x,
+// + gridDim.x, ...  The first two k-tiles of the next output tile are
+// loaded while the current tile's epilogue runs.
 template <int BM, int BN, bool AK, bool BKM, int EPI, bool OUTF32>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
   using C = TileCfg<BM, BN, AK, BKM>;
@@ -234,177 +301,183 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
   __shared__ __attribute__((aligned(1024))) char smem[C::LDS_BYTES];
 
   const int nbm = (g.M + BM - 1) / BM, nbn = (g.N + BN - 1) / BN;
-  int tm, tn;
-  tile_of_block(nbm, nbn, tm, tn);
-  const int zs = blockIdx.z % g.ksplit;
-  const int zb = blockIdx.z / g.ksplit;
-  const int m0 = tm * BM, n0 = tn * BN;
-  const bf16_t* __restrict__ A = (const bf16_t*)g.A + batch_off(zb, g.zdiv, g.sA1, g.sA2);
-  const bf16_t* __restrict__ B = (const bf16_t*)g.B + batch_off(zb, g.zdiv, g.sB1, g.sB2);
-  const int kbeg = zs * g.kchunk;
-  const int kend = min(g.K, kbeg + g.kchunk);
-
+  const int total = nbm * nbn * g.zdiv_total;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int hf = lane >> 5, rr = lane & 31;
-
-  // Buffer resources.  k-major: from the tile's first row to the operand's
-  // last row (rows past it read 0; K is a multiple of 64).  m/n-major: from
-  // this split's first k-row and the tile's first column to the end of the
-  // operand (k-rows past K read 0).  Reads past the valid columns of a
-  // m/n-major row only feed output rows/columns that are never stored.
-  __amdgpu_buffer_rsrc_t rsA, rsB;
-  int kA0, kB0;
-  if constexpr (AK) {
-    rsA = make_rsrc(A + (int64_t)m0 * g.lda, (int64_t)(g.M - m0) * g.lda * 2);
-    kA0 = kbeg;
-  } else {
-    rsA = make_rsrc(A + (int64_t)kbeg * g.lda + m0, ((int64_t)(g.K - kbeg) * g.lda - m0) * 2);
-    kA0 = 0;
-  }
-  if constexpr (BKM) {
-    rsB = make_rsrc(B + (int64_t)n0 * g.ldb, (int64_t)(g.N - n0) * g.ldb * 2);
-    kB0 = kbeg;
-  } else {
-    rsB = make_rsrc(B + (int64_t)kbeg * g.ldb + n0, ((int64_t)(g.K - kbeg) * g.ldb - n0) * 2);
-    kB0 = 0;
-  }
-
-  f32x16_t acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-
-  const int ntiles = (kend - kbeg + BK - 1) / BK;
   constexpr int KS = BK / 16;
   // s_waitcnt immediates (gfx9 encoding: vmcnt[3:0] | expcnt[6:4] |
-  // lgkmcnt[11:8] | vmcnt[5:4] << 14): "vmcnt <= one k-tile of this
-  // wavefront's direct-to-LDS loads" and "vmcnt = 0 and lgkmcnt = 0".
-  constexpr int NDMA = BM / 32 + BN / 32;
-  constexpr int WAIT_ONE_TILE_IN_FLIGHT = (NDMA & 15) | ((NDMA >> 4) << 14) | 0x0F70;
+  // lgkmcnt[11:8] | vmcnt[5:4] << 14): "vmcnt = 0 and lgkmcnt = 0".
   constexpr int WAIT_ALL = 0x0070;
 
-  // Prologue: tiles 0 and 1 in flight, wait for tile 0.
-  bf16x8_t af[2][TM], bfr[2][TN];
-  if (ntiles > 0) {
-    dma_tile<BM, AK>(rsA, g.lda, kA0, smem, wave, lane);
-    dma_tile<BN, BKM>(rsB, g.ldb, kB0, smem + C::A_BYTES, wave, lane);
-    if (ntiles > 1) {
-      dma_tile<BM, AK>(rsA, g.lda, kA0 + BK, smem + C::STAGE_BYTES, wave, lane);
-      dma_tile<BN, BKM>(rsB, g.ldb, kB0 + BK, smem + C::STAGE_BYTES + C::A_BYTES, wave, lane);
-      __builtin_amdgcn_s_waitcnt(WAIT_ONE_TILE_IN_FLIGHT);
-    } else {
-      __builtin_amdgcn_s_waitcnt(WAIT_ALL);
-    }
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < TM; ++i) af[0][i] = frag<BM, AK>(smem, wm * C::WM + i * 32, 0, lane);
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-      bfr[0][j] = frag<BN, BKM>(smem + C::A_BYTES, wn * C::WN + j * 32, 0, lane);
+  int vt = blockIdx.x;
+  if (vt >= total) return;
+  TileOps T = tile_ops<BM, BN, AK, BKM>(g, vt, total, nbm, nbn);
+  // First k-tiles of the first output tile.
+  if (T.ntiles > 0) {
+    dma_tile<BM, AK>(T.rsA, g.lda, T.kA0, smem, wave, lane);
+    dma_tile<BN, BKM>(T.rsB, g.ldb, T.kB0, smem + C::A_BYTES, wave, lane);
   }
-  // Main loop.  While the MFMAs of k-step ks run, the fragments of ks + 1 are
-  // read; in the last k-step of a tile the fragments come from the next tile
-  // instead: wait for this wavefront's loads of tile t + 1 and its reads of
-  // tile t, barrier (every wavefront's tile t + 1 has landed and nobody reads
-  // tile t's buffer any more), refill that buffer with tile t + 2, then read.
-  for (int t = 0; t < ntiles; ++t) {
-    const char* As = smem + (t & 1) * C::STAGE_BYTES;
-    const char* Bs = As + C::A_BYTES;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const int cur = ks & 1, nxt = cur ^ 1;
-      if (ks + 1 < KS) {
-#pragma unroll
-        for (int i = 0; i < TM; ++i) af[nxt][i] = frag<BM, AK>(As, wm * C::WM + i * 32, ks + 1, lane);
-#pragma unroll
-        for (int j = 0; j < TN; ++j) bfr[nxt][j] = frag<BN, BKM>(Bs, wn * C::WN + j * 32, ks + 1, lane);
-      } else if (t + 1 < ntiles) {
-        __builtin_amdgcn_s_waitcnt(WAIT_ALL);
-        __syncthreads();
-        if (t + 2 < ntiles) {
-          char* nb = smem + (t & 1) * C::STAGE_BYTES;
-          dma_tile<BM, AK>(rsA, g.lda, kA0 + (t + 2) * BK, nb, wave, lane);
-          dma_tile<BN, BKM>(rsB, g.ldb, kB0 + (t + 2) * BK, nb + C::A_BYTES, wave, lane);
-        }
-        const char* An = smem + ((t + 1) & 1) * C::STAGE_BYTES;
-#pragma unroll
-        for (int i = 0; i < TM; ++i) af[nxt][i] = frag<BM, AK>(An, wm * C::WM + i * 32, 0, lane);
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          bfr[nxt][j] = frag<BN, BKM>(An + C::A_BYTES, wn * C::WN + j * 32, 0, lane);
-      }
-      // Keep the scheduler from sinking the fragment reads down to their
-      // uses: they must be in flight while these MFMAs execute.
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] =
-              __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+  if (T.ntiles > 1) {
+    dma_tile<BM, AK>(T.rsA, g.lda, T.kA0 + BK, smem + C::STAGE_BYTES, wave, lane);
+    dma_tile<BN, BKM>(T.rsB, g.ldb, T.kB0 + BK, smem + C::STAGE_BYTES + C::A_BYTES, wave, lane);
   }
-  __syncthreads();  // the epilogue reuses the LDS
 
-  // Epilogue.  32x32 accumulator layout: lane holds column (lane % 32);
-  // register r holds row 8 * (r / 4) + 4 * (lane / 32) + (r % 4).
-  const int64_t offC = batch_off(zb, g.zdiv, g.sC1, g.sC2);
-  float* stg = (float*)smem + wave * 32 * C::EPI_LD;
-  const int mw = m0 + wm * C::WM, nw = n0 + wn * C::WN;
-  constexpr int CH = C::WN / 8;  // 8-column chunks per staged row
-  // Optional column sums (EPI_MUL): every lane keeps one 8-column chunk
-  // (CH divides 64) over the rows it writes.
-  constexpr bool COLSUM = EPI == EPI_MUL && CH == 16 && C::WM == 128;
-  float csum[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (;;) {
+    f32x16_t acc[TM][TN];
 #pragma unroll
-  for (int i = 0; i < TM; ++i) {
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+      for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        stg[(8 * (r >> 2) + 4 * hf + (r & 3)) * C::EPI_LD + j * 32 + rr] = acc[i][j][r];
-    __builtin_amdgcn_wave_barrier();
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    const int ntiles = T.ntiles;
+
+    // k-tiles 0 and 1 are in flight (issued before the previous epilogue or
+    // above); wait for everything outstanding, then read k-tile 0.
+    bf16x8_t af[2][TM], bfr[2][TN];
+    __builtin_amdgcn_s_waitcnt(WAIT_ALL);
+    __syncthreads();
+    if (ntiles > 0) {
 #pragma unroll
-    for (int q = 0; q < 32 * CH / 64; ++q) {
-      const int c = lane + 64 * q;
-      const int row = c / CH, col = (c % CH) * 8;
-      const int m = mw + i * 32 + row, n = nw + col;
-      float v[8];
-      const f32x4_t x0 = *(const f32x4_t*)(stg + row * C::EPI_LD + col);
-      const f32x4_t x1 = *(const f32x4_t*)(stg + row * C::EPI_LD + col + 4);
+      for (int i = 0; i < TM; ++i) af[0][i] = frag<BM, AK>(smem, wm * C::WM + i * 32, 0, lane);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        v[e] = x0[e];
-        v[4 + e] = x1[e];
-      }
-      if (m < g.M && n < g.N) {
-        epi8<EPI, OUTF32>(g, offC, zs, m, n, v);
-        if (COLSUM) {
+      for (int j = 0; j < TN; ++j)
+        bfr[0][j] = frag<BN, BKM>(smem + C::A_BYTES, wn * C::WN + j * 32, 0, lane);
+    }
+    // Main loop.  While the MFMAs of k-step ks run, the fragments of ks + 1
+    // are read; in the last k-step of a k-tile they come from the next
+    // k-tile instead: wait for this wavefront's loads of k-tile t + 1 and
+    // its reads of k-tile t, barrier (every wavefront's k-tile t + 1 has
+    // landed and nobody reads k-tile t's buffer any more), refill that
+    // buffer with k-tile t + 2, then read.
+    for (int t = 0; t < ntiles; ++t) {
+      const char* As = smem + (t & 1) * C::STAGE_BYTES;
+      const char* Bs = As + C::A_BYTES;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) csum[e] += v[e];
+      for (int ks = 0; ks < KS; ++ks) {
+        const int cur = ks & 1, nxt = cur ^ 1;
+        if (ks + 1 < KS) {
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+            af[nxt][i] = frag<BM, AK>(As, wm * C::WM + i * 32, ks + 1, lane);
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            bfr[nxt][j] = frag<BN, BKM>(Bs, wn * C::WN + j * 32, ks + 1, lane);
+        } else if (t + 1 < ntiles) {
+          __builtin_amdgcn_s_waitcnt(WAIT_ALL);
+          __syncthreads();
+          if (t + 2 < ntiles) {
+            char* nb = smem + (t & 1) * C::STAGE_BYTES;
+            dma_tile<BM, AK>(T.rsA, g.lda, T.kA0 + (t + 2) * BK, nb, wave, lane);
+            dma_tile<BN, BKM>(T.rsB, g.ldb, T.kB0 + (t + 2) * BK, nb + C::A_BYTES, wave, lane);
+          }
+          const char* An = smem + ((t + 1) & 1) * C::STAGE_BYTES;
+#pragma unroll
+          for (int i = 0; i < TM; ++i) af[nxt][i] = frag<BM, AK>(An, wm * C::WM + i * 32, 0, lane);
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            bfr[nxt][j] = frag<BN, BKM>(An + C::A_BYTES, wn * C::WN + j * 32, 0, lane);
         }
+        // Keep the scheduler from sinking the fragment reads down to their
+        // uses: they must be in flight while these MFMAs execute.
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j],
+                                                                acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
-    __builtin_amdgcn_wave_barrier();
-  }
-  if (COLSUM && g.colpart) {
-    // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same columns: fixed-order sum
+
+    // Every wavefront has read its last fragments: both stages are free.
+    // Start the next output tile's first two k-tiles, then run this tile's
+    // epilogue (its staging area is separate from the stages).
+    __syncthreads();
+    const int m0 = T.m0, n0 = T.n0, zs = T.zs, zb = T.zb;
+    vt += gridDim.x;
+    const bool more = vt < total;
+    if (more) {
+      T = tile_ops<BM, BN, AK, BKM>(g, vt, total, nbm, nbn);
+      if (T.ntiles > 0) {
+        dma_tile<BM, AK>(T.rsA, g.lda, T.kA0, smem, wave, lane);
+        dma_tile<BN, BKM>(T.rsB, g.ldb, T.kB0, smem + C::A_BYTES, wave, lane);
+      }
+      if (T.ntiles > 1) {
+        dma_tile<BM, AK>(T.rsA, g.lda, T.kA0 + BK, smem + C::STAGE_BYTES, wave, lane);
+        dma_tile<BN, BKM>(T.rsB, g.ldb, T.kB0 + BK, smem + C::STAGE_BYTES + C::A_BYTES, wave,
+                          lane);
+      }
+    }
+
+    // Epilogue.  32x32 accumulator layout: lane holds column (lane % 32);
+    // register r holds row 8 * (r / 4) + 4 * (lane / 32) + (r % 4).  Each
+    // 16-row half (registers 0-7, 8-15) of a 32-row slab is staged through
+    // the wavefront's LDS area as fp32; columns are XOR-swizzled by 32 on
+    // rows 4-7 / 12-15 so the two lane halves' stores hit different banks.
+    const int64_t offC = batch_off(zb, g.zdiv, g.sC1, g.sC2);
+    float* stg = (float*)(smem + 2 * C::STAGE_BYTES) + wave * 16 * C::WN;
+    const int mw = m0 + wm * C::WM, nw = n0 + wn * C::WN;
+    constexpr int CH = C::WN / 8;  // 8-column chunks per staged row
+    // Optional column sums (EPI_MUL): every lane keeps one 8-column chunk
+    // (CH divides 64) over the rows it writes.
+    constexpr bool COLSUM = EPI == EPI_MUL && CH == 16 && C::WM == 128;
+    float csum[8] = {0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      csum[e] += __shfl_xor(csum[e], 16, 64);
-      csum[e] += __shfl_xor(csum[e], 32, 64);
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 8 * half; r < 8 * half + 8; ++r) {
+            const int row = 8 * ((r >> 2) & 1) + 4 * hf + (r & 3);  // 0..15
+            const int col = (j * 32 + rr) ^ (hf * 32);
+            stg[row * C::WN + col] = acc[i][j][r];
+          }
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int q = 0; q < 16 * CH / 64; ++q) {
+          const int c = lane + 64 * q;
+          const int row = c / CH, col = (c % CH) * 8;
+          const int pcol = col ^ (((row >> 2) & 1) * 32);
+          const int m = mw + i * 32 + 16 * half + row, n = nw + col;
+          float v[8];
+          const f32x4_t x0 = *(const f32x4_t*)(stg + row * C::WN + pcol);
+          const f32x4_t x1 = *(const f32x4_t*)(stg + row * C::WN + pcol + 4);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[e] = x0[e];
+            v[4 + e] = x1[e];
+          }
+          if (m < g.M && n < g.N) {
+            epi8<EPI, OUTF32>(g, offC, zs, m, n, v);
+            if (COLSUM) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) csum[e] += v[e];
+            }
+          }
+        }
+        __builtin_amdgcn_wave_barrier();
+      }
     }
-    const int n = nw + (lane & 15) * 8;
-    if (lane < 16 && n < g.N) {
-      float* P = g.colpart + (int64_t)(mw / C::WM) * g.N + n;
-      *(f32x4_t*)P = f32x4_t{csum[0], csum[1], csum[2], csum[3]};
-      *(f32x4_t*)(P + 4) = f32x4_t{csum[4], csum[5], csum[6], csum[7]};
+    if (COLSUM && g.colpart) {
+      // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same columns: fixed-order sum
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        csum[e] += __shfl_xor(csum[e], 16, 64);
+        csum[e] += __shfl_xor(csum[e], 32, 64);
+      }
+      const int n = nw + (lane & 15) * 8;
+      if (lane < 16 && n < g.N) {
+        float* P = g.colpart + (int64_t)(mw / C::WM) * g.N + n;
+        *(f32x4_t*)P = f32x4_t{csum[0], csum[1], csum[2], csum[3]};
+        *(f32x4_t*)(P + 4) = f32x4_t{csum[4], csum[5], csum[6], csum[7]};
+      }
     }
+    if (!more) break;
   }
 }
 
@@ -502,11 +575,29 @@ __global__ void splitk_reduce_kernel(const float* __restrict__ part, int splits,
   out[i] = s;
 }
 
+int device_cus() {
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cus = n;
+  }
+  return cus;
+}
+
 template <int BM, int BN, bool AK, bool BKM, int EPI, bool OUTF32>
-hipError_t launch_bf16(const GemmArgs& g, int batch, hipStream_t st) {
-  int nbm = (g.M + BM - 1) / BM, nbn = (g.N + BN - 1) / BN;
-  dim3 grid(nbm * nbn, 1, batch * g.ksplit);
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, AK, BKM, EPI, OUTF32>), grid, dim3(NT), 0, st, g);
+hipError_t launch_bf16(const GemmArgs& g0, int batch, hipStream_t st) {
+  GemmArgs g = g0;
+  g.zdiv_total = batch * g.ksplit;
+  const int64_t total = (int64_t)((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN) * g.zdiv_total;
+  // One work-group per CU (LDS and registers allow no more); a multiple of
+  // 8 so that each work-group stays on one XCD's share of the tiles.
+  int64_t grid = std::min<int64_t>(total, device_cus());
+  if (grid >= 8) grid -= grid % 8;
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, AK, BKM, EPI, OUTF32>), dim3((unsigned)grid),
+                     dim3(NT), 0, st, g);
   return hipGetLastError();
 }
 

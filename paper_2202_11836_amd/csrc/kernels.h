@@ -42,6 +42,7 @@ struct GemmArgs {
   // EPI_MUL on bf16, optional: column sums of the stored output per block
   // of 128 rows, colpart[m / 128][n] (needs tile 1).
   float* colpart;
+  int zdiv_total;  // internal: batch * ksplit
 };
 
 inline GemmArgs gemm_args(const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
