@@ -124,7 +124,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const T* __restrict__ dy,
                                                      const float* __restrict__ gamma,
                                                      T* __restrict__ dz, float* __restrict__ part,
                                                      int rows, int h, int rpb) {
-  extern __shared__ float red[];  // [3][h]
+  extern __shared__ float red[];  // [4 wavefronts][3][h]
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int nchunk = h >> 3;
@@ -139,73 +139,88 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const T* __restrict__ dy,
   const int r0 = blockIdx.x * rpb;
   const int r1 = min(rows, r0 + rpb);
   const float inv_h = 1.0f / (float)h;
-  for (int row = r0 + wave; row < r1; row += 4) {
-    const int64_t base = (int64_t)row * h;
-    float dv[NC][8], xv[NC][8];
-    float sg = 0.0f, sgx = 0.0f;
+  // Two rows per wavefront at a time (rows row and row + 4), so that the
+  // loads of both are in flight together.
+  for (int row0 = r0 + wave; row0 < r1; row0 += 8) {
+    float dv[2][NC][8], xv[2][NC][8];
+    float sg[2] = {0.0f, 0.0f}, sgx[2] = {0.0f, 0.0f};
 #pragma unroll
-    for (int i = 0; i < NC; ++i) {
-      const int c = lane + 64 * i;
-      if (c < nchunk) {
-        load8(dy + base + 8 * c, dv[i]);
-        load8(xhat + base + 8 * c, xv[i]);
+    for (int u = 0; u < 2; ++u) {
+      const int row = row0 + 4 * u;
+      const int64_t base = (int64_t)row * h;
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          float g = dv[i][k] * gm[i][k];
-          sg += g;
-          sgx += g * xv[i][k];
-          pg[i][k] += dv[i][k] * xv[i][k];
-          pb[i][k] += dv[i][k];
+      for (int i = 0; i < NC; ++i) {
+        const int c = lane + 64 * i;
+        if (c < nchunk && row < r1) {
+          load8(dy + base + 8 * c, dv[u][i]);
+          load8(xhat + base + 8 * c, xv[u][i]);
+        } else {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) dv[u][i][k] = xv[u][i][k] = 0.0f;
         }
       }
     }
-    sg = wave_sum(sg) * inv_h;
-    sgx = wave_sum(sgx) * inv_h;
-    const float r = rstd[row];
 #pragma unroll
-    for (int i = 0; i < NC; ++i) {
-      const int c = lane + 64 * i;
-      if (c < nchunk) {
-        float d[8];
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int i = 0; i < NC; ++i)
 #pragma unroll
         for (int k = 0; k < 8; ++k) {
-          d[k] = r * (dv[i][k] * gm[i][k] - sg - xv[i][k] * sgx);
-          // The column sum uses the value as stored, so that the bias
-          // gradient of the preceding linear layer matches the gradient
-          // that flows on.
-          pz[i][k] += as_stored(d[k], dz);
+          const float g = dv[u][i][k] * gm[i][k];
+          sg[u] += g;
+          sgx[u] += g * xv[u][i][k];
+          pg[i][k] += dv[u][i][k] * xv[u][i][k];
+          pb[i][k] += dv[u][i][k];
         }
-        store8(dz + base + 8 * c, d);
-      }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      sg[u] = wave_sum(sg[u]) * inv_h;
+      sgx[u] = wave_sum(sgx[u]) * inv_h;
     }
-  }
-  // Fixed-order combination of the 4 wavefronts' partials.
-  for (int w = 0; w < 4; ++w) {
-    if (wave == w) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int row = row0 + 4 * u;
+      if (row >= r1) continue;
+      const int64_t base = (int64_t)row * h;
+      const float rs = rstd[row];
 #pragma unroll
       for (int i = 0; i < NC; ++i) {
         const int c = lane + 64 * i;
         if (c < nchunk) {
+          float d[8];
 #pragma unroll
           for (int k = 0; k < 8; ++k) {
-            const int col = 8 * c + k;
-            if (w == 0) {
-              red[col] = pg[i][k];
-              red[h + col] = pb[i][k];
-              red[2 * h + col] = pz[i][k];
-            } else {
-              red[col] += pg[i][k];
-              red[h + col] += pb[i][k];
-              red[2 * h + col] += pz[i][k];
-            }
+            d[k] = rs * (dv[u][i][k] * gm[i][k] - sg[u] - xv[u][i][k] * sgx[u]);
+            // The column sum uses the value as stored, so that the bias
+            // gradient of the preceding linear layer matches the gradient
+            // that flows on.
+            pz[i][k] += as_stored(d[k], dz);
           }
+          store8(dz + base + 8 * c, d);
         }
       }
     }
-    __syncthreads();
   }
+  // Each wavefront parks its partials in LDS; after one barrier every
+  // thread sums the 4 wavefronts' values of its columns in a fixed order.
+  float* mine = red + wave * 3 * h;
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int c = lane + 64 * i;
+    if (c < nchunk) {
+      const int col = 8 * c;
+      *(f32x4_t*)(mine + col) = f32x4_t{pg[i][0], pg[i][1], pg[i][2], pg[i][3]};
+      *(f32x4_t*)(mine + col + 4) = f32x4_t{pg[i][4], pg[i][5], pg[i][6], pg[i][7]};
+      *(f32x4_t*)(mine + h + col) = f32x4_t{pb[i][0], pb[i][1], pb[i][2], pb[i][3]};
+      *(f32x4_t*)(mine + h + col + 4) = f32x4_t{pb[i][4], pb[i][5], pb[i][6], pb[i][7]};
+      *(f32x4_t*)(mine + 2 * h + col) = f32x4_t{pz[i][0], pz[i][1], pz[i][2], pz[i][3]};
+      *(f32x4_t*)(mine + 2 * h + col + 4) = f32x4_t{pz[i][4], pz[i][5], pz[i][6], pz[i][7]};
+    }
+  }
+  __syncthreads();
   float* P = part + (int64_t)blockIdx.x * 3 * h;
-  for (int e = threadIdx.x; e < 3 * h; e += 256) P[e] = red[e];
+  for (int e = threadIdx.x; e < 3 * h; e += 256)
+    P[e] = ((red[e] + red[3 * h + e]) + red[6 * h + e]) + red[9 * h + e];
 }
 
 template <typename T>
@@ -354,7 +369,7 @@ hipError_t ln_bwd(const T* dy, const T* xhat, const float* rstd, const float* ga
   if (rows <= 0) return hipSuccess;
   const int nc = (h / 8 + 63) / 64;
   dim3 grid(ln_bwd_blocks(rows)), blk(256);
-  size_t sh = (size_t)3 * h * sizeof(float);
+  size_t sh = (size_t)4 * 3 * h * sizeof(float);
   const int rpb = LN_BWD_RPB;
   switch (nc) {
     case 1: hipLaunchKernelGGL((ln_bwd_kernel<T, 1>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
