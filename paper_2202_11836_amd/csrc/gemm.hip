@@ -171,7 +171,7 @@ __device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
 // For EPI_MUL, v returns the values as stored.
 template <int EPI, bool OUTF32>
 __device__ __forceinline__ void epi8(const GemmArgs& g, int64_t offC, int zs, int m, int n,
-                                     float v[8]) {
+                                     float v[8], u32x4_t x) {
   const int64_t idx = (int64_t)m * g.ldc + n;
   if (EPI == EPI_PARTIAL) {
     float* C = (float*)g.C + (int64_t)zs * g.M * g.ldc + idx;
@@ -200,7 +200,6 @@ __device__ __forceinline__ void epi8(const GemmArgs& g, int64_t offC, int zs, in
     return;
   }
   if (EPI == EPI_MUL || EPI == EPI_RESID) {
-    const u32x4_t x = *(const u32x4_t*)((const bf16_t*)g.aux + offC + (int64_t)m * g.ldaux + n);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const float a0 = __uint_as_float(x[i] << 16), a1 = __uint_as_float(x[i] & 0xffff0000u);
@@ -397,6 +396,27 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
     // epilogue (its staging area is separate from the stages).
     __syncthreads();
     const int m0 = T.m0, n0 = T.n0, zs = T.zs, zb = T.zb;
+    const int64_t offC = batch_off(zb, g.zdiv, g.sC1, g.sC2);
+    const int mw = m0 + wm * C::WM, nw = n0 + wn * C::WN;
+    constexpr int CH = C::WN / 8;  // 8-column chunks per staged row
+    constexpr int QN = 16 * CH / 64;  // chunks per lane per staged 16-row half
+    // EPI_MUL / EPI_RESID read one bf16 operand chunk per output chunk; the
+    // chunks of the next staged half are loaded while this one is processed
+    // (the first ones before the next tile's k-tiles are requested).
+    constexpr bool AUX = EPI == EPI_MUL || EPI == EPI_RESID;
+    u32x4_t axv[2][QN];
+    auto aux_load = [&](int it, u32x4_t* dst) {
+#pragma unroll
+      for (int q = 0; q < QN; ++q) {
+        const int c = lane + 64 * q;
+        const int row = c / CH, col = (c % CH) * 8;
+        const int m = mw + (it >> 1) * 32 + 16 * (it & 1) + row, n = nw + col;
+        dst[q] = (m < g.M && n < g.N)
+                     ? *(const u32x4_t*)((const bf16_t*)g.aux + offC + (int64_t)m * g.ldaux + n)
+                     : u32x4_t{0, 0, 0, 0};
+      }
+    };
+    if constexpr (AUX) aux_load(0, axv[0]);
     vt += gridDim.x;
     const bool more = vt < total;
     if (more) {
@@ -417,10 +437,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
     // 16-row half (registers 0-7, 8-15) of a 32-row slab is staged through
     // the wavefront's LDS area as fp32; columns are XOR-swizzled by 32 on
     // rows 4-7 / 12-15 so the two lane halves' stores hit different banks.
-    const int64_t offC = batch_off(zb, g.zdiv, g.sC1, g.sC2);
     float* stg = (float*)(smem + 2 * C::STAGE_BYTES) + wave * 16 * C::WN;
-    const int mw = m0 + wm * C::WM, nw = n0 + wn * C::WN;
-    constexpr int CH = C::WN / 8;  // 8-column chunks per staged row
     // Optional column sums (EPI_MUL): every lane keeps one 8-column chunk
     // (CH divides 64) over the rows it writes.
     constexpr bool COLSUM = EPI == EPI_MUL && CH == 16 && C::WM == 128;
@@ -429,6 +446,10 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
+        const int it = 2 * i + half;
+        if constexpr (AUX) {
+          if (it + 1 < 2 * TM) aux_load(it + 1, axv[(it + 1) & 1]);
+        }
 #pragma unroll
         for (int j = 0; j < TN; ++j)
 #pragma unroll
@@ -439,7 +460,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
           }
         __builtin_amdgcn_wave_barrier();
 #pragma unroll
-        for (int q = 0; q < 16 * CH / 64; ++q) {
+        for (int q = 0; q < QN; ++q) {
           const int c = lane + 64 * q;
           const int row = c / CH, col = (c % CH) * 8;
           const int pcol = col ^ (((row >> 2) & 1) * 32);
@@ -453,7 +474,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
             v[4 + e] = x1[e];
           }
           if (m < g.M && n < g.N) {
-            epi8<EPI, OUTF32>(g, offC, zs, m, n, v);
+            epi8<EPI, OUTF32>(g, offC, zs, m, n, v, AUX ? axv[it & 1][q] : u32x4_t{0, 0, 0, 0});
             if (COLSUM) {
 #pragma unroll
               for (int e = 0; e < 8; ++e) csum[e] += v[e];

@@ -240,24 +240,26 @@ struct OutPtrs {
   float* p[4];
 };
 
-// 64 columns x 16 stripes of partial rows per block; the 16 stripe sums are
-// combined in LDS by a fixed-order tree.
-__global__ __launch_bounds__(1024) void col_reduce_kernel(const float* __restrict__ part, int nblk,
-                                                          int nvec, int n, OutPtrs outs) {
-  __shared__ float sm[16][65];
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  const int c = blockIdx.x * 64 + tx;
+// 16 columns per block: 4 threads x 4 columns per partial row, 64 stripes of
+// partial rows; the stripe sums are combined in LDS by a fixed-order tree.
+__global__ __launch_bounds__(256) void col_reduce_kernel(const float* __restrict__ part, int nblk,
+                                                         int nvec, int n, OutPtrs outs) {
+  __shared__ f32x4_t sm[64][4];
+  const int q = threadIdx.x & 3, stripe = threadIdx.x >> 2;
+  const int c = blockIdx.x * 16 + 4 * q;
   const int v = blockIdx.y;
-  float s = 0.0f;
-  if (c < n)
-    for (int b = ty; b < nblk; b += 16) s += part[((int64_t)b * nvec + v) * n + c];
-  sm[ty][tx] = s;
+  f32x4_t s = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (c < n) {
+#pragma unroll 8
+    for (int b = stripe; b < nblk; b += 64) s += *(const f32x4_t*)(part + ((int64_t)b * nvec + v) * n + c);
+  }
+  sm[stripe][q] = s;
   __syncthreads();
-  for (int w = 8; w > 0; w >>= 1) {
-    if (ty < w) sm[ty][tx] += sm[ty + w][tx];
+  for (int w = 32; w > 0; w >>= 1) {
+    if (stripe < w) sm[stripe][q] += sm[stripe + w][q];
     __syncthreads();
   }
-  if (ty == 0 && c < n && outs.p[v]) outs.p[v][c] = sm[0][tx];
+  if (stripe == 0 && c < n && outs.p[v]) *(f32x4_t*)(outs.p[v] + c) = sm[0][q];
 }
 
 // P = softmax over keys of scale * scores, masked keys -> 0, empty rows -> 0.
@@ -314,28 +316,58 @@ __global__ __launch_bounds__(256) void softmax_bwd_kernel(const float* __restric
 }
 
 // dst[c][r] = src[r][c] for a bf16 [R][C] matrix; 64 x 64 tiles through LDS.
-__global__ __launch_bounds__(256) void transpose_bf16_kernel(const bf16_t* __restrict__ src, int R,
-                                                             int C, bf16_t* __restrict__ dst) {
-  __shared__ bf16_t t[64][66];
-  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int i = ty; i < 64; i += 4) {
-    const int r = r0 + i, c = c0 + tx;
-    t[i][tx] = (r < R && c < C) ? src[(int64_t)r * C + c] : (bf16_t)0;
+// Batched bf16 transpose dst[c][r] = src[r][c] over 64 x 64 tiles; rows and
+// columns are multiples of 8 so HBM is read and written in 16-byte pieces.
+// Work-group b handles tile b - job.tile0 of the job whose range holds b.
+__global__ __launch_bounds__(256) void transpose_bf16_kernel(TransposeBatch jb) {
+  __shared__ __attribute__((aligned(16))) bf16_t t[64][72];
+  int k = 0;
+  while (k + 1 < jb.n && (int)blockIdx.x >= jb.job[k + 1].tile0) ++k;
+  const TransposeJob J = jb.job[k];
+  const int tiles_c = (J.C + 63) / 64;
+  const int tile = blockIdx.x - J.tile0;
+  const int r0 = (tile / tiles_c) * 64, c0 = (tile % tiles_c) * 64;
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    const int idx = threadIdx.x + 256 * p;
+    const int row = idx >> 3, ch = idx & 7;
+    const int r = r0 + row, c = c0 + 8 * ch;
+    u32x4_t v = {0, 0, 0, 0};
+    if (r < J.R && c < J.C) v = *(const u32x4_t*)(J.src + (int64_t)r * J.C + c);
+    *(u32x4_t*)&t[row][8 * ch] = v;
   }
   __syncthreads();
-  for (int i = ty; i < 64; i += 4) {
-    const int c = c0 + i, r = r0 + tx;
-    if (c < C && r < R) dst[(int64_t)c * R + r] = t[tx][i];
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    const int idx = threadIdx.x + 256 * p;
+    const int orow = idx >> 3, ch = idx & 7;  // output row = source column c0 + orow
+    const int c = c0 + orow, r = r0 + 8 * ch;
+    if (c < J.C && r < J.R) {
+      u32x4_t o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        o[e] = (uint32_t)t[8 * ch + 2 * e][orow] | ((uint32_t)t[8 * ch + 2 * e + 1][orow] << 16);
+      *(u32x4_t*)(J.dst + (int64_t)c * J.R + r) = o;
+    }
   }
 }
 
 }  // namespace
 
-hipError_t transpose_bf16(const bf16_t* src, int R, int C, bf16_t* dst, hipStream_t st) {
-  if (R <= 0 || C <= 0) return hipSuccess;
-  hipLaunchKernelGGL(transpose_bf16_kernel, dim3((C + 63) / 64, (R + 63) / 64), dim3(256), 0, st,
-                     src, R, C, dst);
+hipError_t transpose_bf16(const TransposeJob* jobs, int n, hipStream_t st) {
+  TransposeBatch b;
+  int tiles = 0;
+  b.n = 0;
+  for (int k = 0; k < n; ++k) {
+    if (jobs[k].R <= 0 || jobs[k].C <= 0) continue;
+    if (jobs[k].R % 8 || jobs[k].C % 8 || b.n == TRANSPOSE_MAX_JOBS) return hipErrorInvalidValue;
+    b.job[b.n] = jobs[k];
+    b.job[b.n].tile0 = tiles;
+    tiles += ((jobs[k].R + 63) / 64) * ((jobs[k].C + 63) / 64);
+    ++b.n;
+  }
+  if (tiles == 0) return hipSuccess;
+  hipLaunchKernelGGL(transpose_bf16_kernel, dim3(tiles), dim3(256), 0, st, b);
   return hipGetLastError();
 }
 
@@ -391,10 +423,11 @@ hipError_t col_partial(const T* x, int rows, int n, float* part, int nblk, hipSt
 
 hipError_t col_reduce(const float* part, int nblk, int nvec, int n, float* const* outs,
                       hipStream_t st) {
-  if (nvec > 4) return hipErrorInvalidValue;
+  if (nvec > 4 || n % 4 != 0) return hipErrorInvalidValue;
+  if (n <= 0 || nvec <= 0) return hipSuccess;
   OutPtrs o{};
   for (int i = 0; i < nvec; ++i) o.p[i] = outs[i];
-  hipLaunchKernelGGL(col_reduce_kernel, dim3((n + 63) / 64, nvec), dim3(1024), 0, st, part, nblk,
+  hipLaunchKernelGGL(col_reduce_kernel, dim3((n + 15) / 16, nvec), dim3(256), 0, st, part, nblk,
                      nvec, n, o);
   return hipGetLastError();
 }

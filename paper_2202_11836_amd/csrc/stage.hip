@@ -514,10 +514,11 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
     const void* W1 = p[STAGE_W_1];
     const void* W2 = p[STAGE_W_2];
     if (kBF) {
-      SITE(WT, transpose_bf16((const bf16_t*)Wq, 3 * h, h, (bf16_t*)s->wt_qkv, st));
-      SITE(WT, transpose_bf16((const bf16_t*)Wo, h, h, (bf16_t*)s->wt_o, st));
-      SITE(WT, transpose_bf16((const bf16_t*)W1, f, h, (bf16_t*)s->wt_1, st));
-      SITE(WT, transpose_bf16((const bf16_t*)W2, h, f, (bf16_t*)s->wt_2, st));
+      const TransposeJob jobs[4] = {{(const bf16_t*)Wq, (bf16_t*)s->wt_qkv, 3 * h, h, 0},
+                                    {(const bf16_t*)Wo, (bf16_t*)s->wt_o, h, h, 0},
+                                    {(const bf16_t*)W1, (bf16_t*)s->wt_1, f, h, 0},
+                                    {(const bf16_t*)W2, (bf16_t*)s->wt_2, h, f, 0}};
+      SITE(WT, transpose_bf16(jobs, 4, st));
       Wq = s->wt_qkv;
       Wo = s->wt_o;
       W1 = s->wt_1;
