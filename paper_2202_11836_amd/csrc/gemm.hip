@@ -76,16 +76,32 @@ __device__ __forceinline__ int64_t batch_off(int zb, int zdiv, int64_t s1, int64
 // residual operands are read and the results written as 16-byte row
 // segments.
 // ---------------------------------------------------------------------------
+// k-tile depth and ring depth per tile shape: a ring of NS k-tiles of BK
+// keeps NS - 1 k-tiles in flight behind the one being consumed.
+// (A deeper ring of k-tiles of 32 was measured slower for 256 x 256: twice
+// the barriers per k, and the loads are not the limit at this depth.)
+template <int BM, int BN>
+struct RingShape {
+  static constexpr int BK = 64;
+  static constexpr int NS = (BM == 256 && BN == 256) ? 2 : (BM == 256 ? 3 : 4);
+};
+
 template <int BM, int BN, bool AK, bool BKM>
 struct TileCfg {
-  static constexpr int BK = 64;
+  static constexpr int BK = RingShape<BM, BN>::BK;
+  static constexpr int NS = RingShape<BM, BN>::NS;
   static constexpr int WM = BM / 2, WN = BN / 2;
   static constexpr int TM = WM / 32, TN = WN / 32;
   static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
   static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
-  // Epilogue staging, beside the two stages: 16 rows x WN fp32 per wavefront.
+  // direct-to-LDS load instructions per k-tile per wavefront (1 KB each)
+  static constexpr int DMA_PER_TILE = STAGE_BYTES / 1024 / 4;
+  // Epilogue staging, beside the ring: 16 rows x WN fp32 per wavefront.
   static constexpr int EPI_BYTES = 4 * 16 * WN * 4;
-  static constexpr int LDS_BYTES = 2 * STAGE_BYTES + EPI_BYTES;
+  static constexpr int LDS_BYTES = NS * STAGE_BYTES + EPI_BYTES;
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
+  static_assert((NS - 2) * DMA_PER_TILE <= 63, "vmcnt range");
+  static_assert(STAGE_BYTES % 4096 == 0, "whole 1 KB blocks per wavefront");
 };
 
 // Buffer resource over [base, base + bytes): loads past the end return 0.
@@ -97,10 +113,11 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, in
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 // LDS tile layouts (no padding; 16-byte chunks XOR-swizzled so that the
-// fragment reads of one pass hit distinct banks):
-//   k-major  [R][64]: row r, logical chunk c (8 k values) at physical chunk
-//            c ^ ((r >> 1) & 7) of the row's 128 bytes;
-//   m/n-major [64][R]: k-row k, logical chunk c (8 rows/columns) at physical
+// fragment reads of each 16-lane group hit distinct banks):
+//   k-major  [R][BK]: row r, logical chunk c (8 k values) at physical chunk
+//            c ^ kswz(r) of the row's 2 BK bytes, kswz(r) = (r >> 1) & 7 for
+//            BK = 64 and (r >> 2) & 3 for BK = 32;
+//   m/n-major [BK][R]: k-row k, logical chunk c (8 rows/columns) at physical
 //            chunk c ^ (4 (k & 3)) of the row's 2R bytes (R >= 128), so the
 //            4 k-rows x 2 chunks of each 16-lane transposing read, and the two
 //            groups of a 32-lane pass, cover 16 distinct chunks.
@@ -110,17 +127,24 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 // of k-tile k0 (k relative to the resource, see the kernel), so the tile
 // never passes through VGPRs.  Each 1 KB block is one instruction; the 4
 // wavefronts split the blocks.
-template <int R, bool KMAJ>
+template <int BK>
+__device__ __forceinline__ int kswz(int r) {
+  return BK == 64 ? ((r >> 1) & 7) : ((r >> 2) & 3);
+}
+
+template <int R, bool KMAJ, int BK>
 __device__ __forceinline__ void dma_tile(__amdgpu_buffer_rsrc_t rs, int64_t ld, int k0, char* dst,
                                          int wave, int lane) {
-  constexpr int NB = R * 64 * 2 / 1024;  // 1 KB blocks in the tile
+  constexpr int NB = R * BK * 2 / 1024;  // 1 KB blocks in the tile
 #pragma unroll
   for (int i = 0; i < NB / 4; ++i) {
     const int q = wave * (NB / 4) + i;
     int64_t elem;
     if constexpr (KMAJ) {
-      const int row = 8 * q + (lane >> 3);
-      const int c = (lane & 7) ^ ((row >> 1) & 7);
+      constexpr int CPR = BK / 8;   // chunks per row
+      constexpr int RPB = 64 / CPR; // rows per block
+      const int row = RPB * q + lane / CPR;
+      const int c = (lane % CPR) ^ kswz<BK>(row);
       elem = (int64_t)row * ld + k0 + 8 * c;
     } else {
       constexpr int CPR = R / 8;           // chunks per k-row
@@ -141,12 +165,12 @@ __device__ __forceinline__ void dma_tile(__amdgpu_buffer_rsrc_t rs, int64_t ld, 
 // receives V[4e + i / 4][i % 4] for e = 0..3.  Lane j of a group points at
 // k-row k0 + j / 4, columns mb + 4 (j % 4), so lane i receives column mb + i
 // at k-rows k0 .. k0 + 3 (the second read: k0 + 4 .. k0 + 7).
-template <int R, bool KMAJ>
+template <int R, bool KMAJ, int BK>
 __device__ __forceinline__ bf16x8_t frag(const char* S, int r0, int ks, int lane) {
   if constexpr (KMAJ) {
     const int r = r0 + (lane & 31);
     const int c = 2 * ks + (lane >> 5);
-    return *(const bf16x8_t*)(S + r * 128 + 16 * (c ^ ((r >> 1) & 7)));
+    return *(const bf16x8_t*)(S + r * (2 * BK) + 16 * (c ^ kswz<BK>(r)));
   } else {
     typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
     const int grp = lane >> 4, j = lane & 15;
@@ -267,7 +291,8 @@ __device__ __forceinline__ TileOps tile_ops(const GemmArgs& g, int vt, int total
   const bf16_t* B = (const bf16_t*)g.B + batch_off(o.zb, g.zdiv, g.sB1, g.sB2);
   const int kbeg = o.zs * g.kchunk;
   const int kend = min(g.K, kbeg + g.kchunk);
-  o.ntiles = (kend - kbeg + 63) / 64;
+  constexpr int BK = TileCfg<BM, BN, AK, BKM>::BK;
+  o.ntiles = (kend - kbeg + BK - 1) / BK;
   // k-major: from the tile's first row to the operand's last row (rows past
   // it read 0; K is a multiple of 64).  m/n-major: from this split's first
   // k-row and the tile's first column to the end of the operand (k-rows past
@@ -290,13 +315,43 @@ __device__ __forceinline__ TileOps tile_ops(const GemmArgs& g, int vt, int total
   return o;
 }
 
+// k-tile t of an output tile -> ring slot t % NS.
+template <int BM, int BN, bool AK, bool BKM>
+__device__ __forceinline__ void issue_ktile(const GemmArgs& g, const TileOps& T, int t, char* smem,
+                                            int wave, int lane) {
+  using C = TileCfg<BM, BN, AK, BKM>;
+  char* b = smem + (t % C::NS) * C::STAGE_BYTES;
+  dma_tile<BM, AK, C::BK>(T.rsA, g.lda, T.kA0 + t * C::BK, b, wave, lane);
+  dma_tile<BN, BKM, C::BK>(T.rsB, g.ldb, T.kB0 + t * C::BK, b + C::A_BYTES, wave, lane);
+}
+
+// s_waitcnt immediate (gfx9 encoding: vmcnt[3:0] | expcnt[6:4] |
+// lgkmcnt[11:8] | vmcnt[5:4] << 14) for "lgkmcnt = 0 and at most N vector
+// memory operations outstanding".
+template <int N>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | 0x70 | (((N >> 4) & 3) << 14));
+}
+
+// Wait until k-tile t + 1 has landed, given that `after` later k-tiles
+// (0 .. NS - 2) have been requested since: the loads complete in order.
+template <int PER, int NS>
+__device__ __forceinline__ void wait_ktile(int after) {
+  if (NS > 5 && after >= 4) wait_vm_lgkm0<(NS > 5 ? 4 * PER : 0)>();
+  else if (NS > 4 && after >= 3) wait_vm_lgkm0<(NS > 4 ? 3 * PER : 0)>();
+  else if (NS > 3 && after >= 2) wait_vm_lgkm0<(NS > 3 ? 2 * PER : 0)>();
+  else if (NS > 2 && after >= 1) wait_vm_lgkm0<(NS > 2 ? PER : 0)>();
+  else wait_vm_lgkm0<0>();
+}
+
 // Persistent kernel: each work-group walks output tiles vt = blockIdx.x,
-// + gridDim.x, ...  The first two k-tiles of the next output tile are
+// + gridDim.x, ...  The first NS k-tiles of the next output tile are
 // loaded while the current tile's epilogue runs.
 template <int BM, int BN, bool AK, bool BKM, int EPI, bool OUTF32>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
   using C = TileCfg<BM, BN, AK, BKM>;
-  constexpr int BK = C::BK, TM = C::TM, TN = C::TN;
+  constexpr int TM = C::TM, TN = C::TN, NS = C::NS;
   __shared__ __attribute__((aligned(1024))) char smem[C::LDS_BYTES];
 
   const int nbm = (g.M + BM - 1) / BM, nbn = (g.N + BN - 1) / BN;
@@ -304,23 +359,15 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int hf = lane >> 5, rr = lane & 31;
-  constexpr int KS = BK / 16;
-  // s_waitcnt immediates (gfx9 encoding: vmcnt[3:0] | expcnt[6:4] |
-  // lgkmcnt[11:8] | vmcnt[5:4] << 14): "vmcnt = 0 and lgkmcnt = 0".
-  constexpr int WAIT_ALL = 0x0070;
+  constexpr int KS = C::BK / 16;
 
   int vt = blockIdx.x;
   if (vt >= total) return;
   TileOps T = tile_ops<BM, BN, AK, BKM>(g, vt, total, nbm, nbn);
   // First k-tiles of the first output tile.
-  if (T.ntiles > 0) {
-    dma_tile<BM, AK>(T.rsA, g.lda, T.kA0, smem, wave, lane);
-    dma_tile<BN, BKM>(T.rsB, g.ldb, T.kB0, smem + C::A_BYTES, wave, lane);
-  }
-  if (T.ntiles > 1) {
-    dma_tile<BM, AK>(T.rsA, g.lda, T.kA0 + BK, smem + C::STAGE_BYTES, wave, lane);
-    dma_tile<BN, BKM>(T.rsB, g.ldb, T.kB0 + BK, smem + C::STAGE_BYTES + C::A_BYTES, wave, lane);
-  }
+#pragma unroll
+  for (int t = 0; t < NS; ++t)
+    if (t < T.ntiles) issue_ktile<BM, BN, AK, BKM>(g, T, t, smem, wave, lane);
 
   for (;;) {
     f32x16_t acc[TM][TN];
@@ -332,26 +379,26 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
     const int ntiles = T.ntiles;
 
-    // k-tiles 0 and 1 are in flight (issued before the previous epilogue or
-    // above); wait for everything outstanding, then read k-tile 0.
+    // The first k-tiles are in flight (issued before the previous epilogue
+    // or above); wait for everything outstanding, then read k-tile 0.
     bf16x8_t af[2][TM], bfr[2][TN];
-    __builtin_amdgcn_s_waitcnt(WAIT_ALL);
+    wait_vm_lgkm0<0>();
     __syncthreads();
     if (ntiles > 0) {
 #pragma unroll
-      for (int i = 0; i < TM; ++i) af[0][i] = frag<BM, AK>(smem, wm * C::WM + i * 32, 0, lane);
+      for (int i = 0; i < TM; ++i) af[0][i] = frag<BM, AK, C::BK>(smem, wm * C::WM + i * 32, 0, lane);
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        bfr[0][j] = frag<BN, BKM>(smem + C::A_BYTES, wn * C::WN + j * 32, 0, lane);
+        bfr[0][j] = frag<BN, BKM, C::BK>(smem + C::A_BYTES, wn * C::WN + j * 32, 0, lane);
     }
     // Main loop.  While the MFMAs of k-step ks run, the fragments of ks + 1
     // are read; in the last k-step of a k-tile they come from the next
     // k-tile instead: wait for this wavefront's loads of k-tile t + 1 and
     // its reads of k-tile t, barrier (every wavefront's k-tile t + 1 has
-    // landed and nobody reads k-tile t's buffer any more), refill that
-    // buffer with k-tile t + 2, then read.
+    // landed and nobody reads k-tile t's slot any more), refill that slot
+    // with k-tile t + NS, then read.
     for (int t = 0; t < ntiles; ++t) {
-      const char* As = smem + (t & 1) * C::STAGE_BYTES;
+      const char* As = smem + (t % NS) * C::STAGE_BYTES;
       const char* Bs = As + C::A_BYTES;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
@@ -359,24 +406,21 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
         if (ks + 1 < KS) {
 #pragma unroll
           for (int i = 0; i < TM; ++i)
-            af[nxt][i] = frag<BM, AK>(As, wm * C::WM + i * 32, ks + 1, lane);
+            af[nxt][i] = frag<BM, AK, C::BK>(As, wm * C::WM + i * 32, ks + 1, lane);
 #pragma unroll
           for (int j = 0; j < TN; ++j)
-            bfr[nxt][j] = frag<BN, BKM>(Bs, wn * C::WN + j * 32, ks + 1, lane);
+            bfr[nxt][j] = frag<BN, BKM, C::BK>(Bs, wn * C::WN + j * 32, ks + 1, lane);
         } else if (t + 1 < ntiles) {
-          __builtin_amdgcn_s_waitcnt(WAIT_ALL);
+          wait_ktile<C::DMA_PER_TILE, NS>(min(ntiles - 1, t + NS - 1) - (t + 1));
           __syncthreads();
-          if (t + 2 < ntiles) {
-            char* nb = smem + (t & 1) * C::STAGE_BYTES;
-            dma_tile<BM, AK>(T.rsA, g.lda, T.kA0 + (t + 2) * BK, nb, wave, lane);
-            dma_tile<BN, BKM>(T.rsB, g.ldb, T.kB0 + (t + 2) * BK, nb + C::A_BYTES, wave, lane);
-          }
-          const char* An = smem + ((t + 1) & 1) * C::STAGE_BYTES;
+          if (t + NS < ntiles) issue_ktile<BM, BN, AK, BKM>(g, T, t + NS, smem, wave, lane);
+          const char* An = smem + ((t + 1) % NS) * C::STAGE_BYTES;
 #pragma unroll
-          for (int i = 0; i < TM; ++i) af[nxt][i] = frag<BM, AK>(An, wm * C::WM + i * 32, 0, lane);
+          for (int i = 0; i < TM; ++i)
+            af[nxt][i] = frag<BM, AK, C::BK>(An, wm * C::WM + i * 32, 0, lane);
 #pragma unroll
           for (int j = 0; j < TN; ++j)
-            bfr[nxt][j] = frag<BN, BKM>(An + C::A_BYTES, wn * C::WN + j * 32, 0, lane);
+            bfr[nxt][j] = frag<BN, BKM, C::BK>(An + C::A_BYTES, wn * C::WN + j * 32, 0, lane);
         }
         // Keep the scheduler from sinking the fragment reads down to their
         // uses: they must be in flight while these MFMAs execute.
@@ -391,9 +435,9 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
       }
     }
 
-    // Every wavefront has read its last fragments: both stages are free.
-    // Start the next output tile's first two k-tiles, then run this tile's
-    // epilogue (its staging area is separate from the stages).
+    // Every wavefront has read its last fragments: the whole ring is free.
+    // Start the next output tile's first NS k-tiles, then run this tile's
+    // epilogue (its staging area is separate from the ring).
     __syncthreads();
     const int m0 = T.m0, n0 = T.n0, zs = T.zs, zb = T.zb;
     const int64_t offC = batch_off(zb, g.zdiv, g.sC1, g.sC2);
@@ -421,15 +465,9 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
     const bool more = vt < total;
     if (more) {
       T = tile_ops<BM, BN, AK, BKM>(g, vt, total, nbm, nbn);
-      if (T.ntiles > 0) {
-        dma_tile<BM, AK>(T.rsA, g.lda, T.kA0, smem, wave, lane);
-        dma_tile<BN, BKM>(T.rsB, g.ldb, T.kB0, smem + C::A_BYTES, wave, lane);
-      }
-      if (T.ntiles > 1) {
-        dma_tile<BM, AK>(T.rsA, g.lda, T.kA0 + BK, smem + C::STAGE_BYTES, wave, lane);
-        dma_tile<BN, BKM>(T.rsB, g.ldb, T.kB0 + BK, smem + C::STAGE_BYTES + C::A_BYTES, wave,
-                          lane);
-      }
+#pragma unroll
+      for (int t = 0; t < NS; ++t)
+        if (t < T.ntiles) issue_ktile<BM, BN, AK, BKM>(g, T, t, smem, wave, lane);
     }
 
     // Epilogue.  32x32 accumulator layout: lane holds column (lane % 32);
@@ -437,7 +475,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
     // 16-row half (registers 0-7, 8-15) of a 32-row slab is staged through
     // the wavefront's LDS area as fp32; columns are XOR-swizzled by 32 on
     // rows 4-7 / 12-15 so the two lane halves' stores hit different banks.
-    float* stg = (float*)(smem + 2 * C::STAGE_BYTES) + wave * 16 * C::WN;
+    float* stg = (float*)(smem + NS * C::STAGE_BYTES) + wave * 16 * C::WN;
     // Optional column sums (EPI_MUL): every lane keeps one 8-column chunk
     // (CH divides 64) over the rows it writes.
     constexpr bool COLSUM = EPI == EPI_MUL && CH == 16 && C::WM == 128;
