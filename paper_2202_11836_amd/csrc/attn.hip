@@ -15,17 +15,24 @@
 // needs them per lane (lane = query, 16 keys in registers), so the
 // statistics and the rescaling of the output are per-lane scalars; the fp32
 // accumulator registers are converted to bf16 and fed straight back as the
-// B operand of the next contraction.  Because a 32x32 accumulator holds rows
-// {8*(r/4) + 4*(lane/32) + r%4}, the matching A operand is read from a
-// transposed LDS tile with that same row permutation (two 8-byte reads).
+// B operand of the next contraction.  The streamed 64-row blocks (keys and
+// values, or queries and output gradients) go from HBM straight into a
+// two-stage LDS ring with direct-to-LDS loads, one block ahead of the one
+// being used.  Their row-major tiles serve both operand shapes: row
+// fragments with 16-byte reads, and the transposed operand that multiplies an
+// accumulator-held matrix with gfx950's transposing LDS read, taking the
+// accumulator's row order {8*(r/4) + 4*(lane/32) + r%4} directly.
+
 #include "kernels.h"
 
 namespace {
 
-constexpr int HD = 64;        // head dimension
-constexpr int KT = 64;        // rows per LDS tile (keys or queries)
-constexpr int LD = HD + 8;    // padded LDS row (elements) of a [row][dim] tile
-constexpr int LDT = KT + 8;   // padded LDS row of a transposed [dim][row] tile
+constexpr int HD = 64;               // head dimension
+constexpr int KT = 64;               // rows per streamed block
+constexpr int TILE = KT * HD * 2;    // bytes of one [64][64] bf16 tile
+constexpr int LD = HD + 8;           // padded row (elements) of the output staging area
+
+typedef __attribute__((address_space(3))) void lds_void_t;
 
 __device__ __forceinline__ f32x16_t mfma32(bf16x8_t a, bf16x8_t b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -51,56 +58,71 @@ __device__ __forceinline__ bf16x8_t pack8(const f32x16_t& a, int r0) {
 
 __device__ __forceinline__ bf16x8_t ld_frag(const bf16_t* p) { return *(const bf16x8_t*)p; }
 
-// A operand from a transposed tile Xt[col][row]: column c, contraction step
-// ks over the 32 rows starting at row0, in the accumulator row order.
-__device__ __forceinline__ bf16x8_t ld_frag_t(const bf16_t* Xt, int c, int row0, int ks, int hf) {
-  const bf16_t* p = Xt + c * LDT + row0 + 16 * ks + 4 * hf;
-  u32x2_t lo = *(const u32x2_t*)p;
-  u32x2_t hi = *(const u32x2_t*)(p + 8);
-  u32x4_t v = {lo[0], lo[1], hi[0], hi[1]};
-  return __builtin_bit_cast(bf16x8_t, v);
-}
-
 __device__ __forceinline__ u32x4_t zero4() { return u32x4_t{0, 0, 0, 0}; }
 
-// Copy rows [r0, r0 + KT) of a [rows][64] bf16 matrix (row stride ld,
-// rows >= nrows read as zero) into the LDS tile X[KT][LD].
-__device__ __forceinline__ void load_rows(const bf16_t* __restrict__ src, int64_t ld, int r0,
-                                          int nrows, bf16_t* X) {
-  const int tid = threadIdx.x;
+// LDS tile [64 rows][64 bf16]: 128-byte rows of 8 16-byte chunks, chunk c of
+// row r stored at chunk c ^ f(u), u = (r >> 1) & 7, f(u) = (u0 << 2) |
+// (u2 << 1) | u1.  The 16 rows of a row-fragment read and the 4 rows x 64
+// bytes of a transposing read then fall on distinct banks.
+__device__ __forceinline__ int tswz(int r) {
+  const int u = (r >> 1) & 7;
+  return ((u & 1) << 2) | (((u >> 2) & 1) << 1) | ((u >> 1) & 1);
+}
+__device__ __forceinline__ int toff(int r, int c) { return r * 128 + 16 * (c ^ tswz(r)); }
+
+// Buffer resource over rows 0 .. n-1 of a [rows][64] bf16 operand with row
+// stride ld elements: loads of later rows return 0.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const bf16_t* base, int n, int64_t ld) {
+  const int64_t bytes = n > 0 ? ((int64_t)(n - 1) * ld + HD) * 2 : 0;
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0,
+                                           (int)(bytes > 0x7fffffff ? 0x7fffffff : bytes),
+                                           0x00020000);
+}
+
+// Rows [row0, row0 + 64) into a tile with direct-to-LDS loads: 8 loads of
+// 8 rows (lane l's 16 bytes land at +16 l), two per wavefront.
+__device__ __forceinline__ void dma_rows(__amdgpu_buffer_rsrc_t rs, int row0, int64_t ld,
+                                         char* tile, int wave, int lane) {
 #pragma unroll
-  for (int i = 0; i < KT * 8 / 256; ++i) {
-    int v = tid + 256 * i;
-    int row = v >> 3, c8 = (v & 7) * 8;
-    u32x4_t val = zero4();
-    if (r0 + row < nrows) val = *(const u32x4_t*)(src + (int64_t)(r0 + row) * ld + c8);
-    *(u32x4_t*)(X + row * LD + c8) = val;
+  for (int i = 0; i < 2; ++i) {
+    const int q = 2 * wave + i;
+    const int r = 8 * q + (lane >> 3);
+    const int c = (lane & 7) ^ tswz(r);
+    const int64_t off = ((int64_t)(row0 + r) * ld + 8 * c) * 2;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)(tile + q * 1024), 16,
+                                             (int)(off > 0x7fffffff ? 0x7fffffff : off), 0, 0, 0);
   }
 }
 
-// Same rows into the transposed LDS tile Xt[64][LDT]: each of 128 threads
-// moves a block of 4 rows x 8 columns and transposes it in registers.
-__device__ __forceinline__ void load_rows_t(const bf16_t* __restrict__ src, int64_t ld, int r0,
-                                            int nrows, bf16_t* Xt) {
-  const int tid = threadIdx.x;
-  if (tid < KT / 4 * 8) {
-    const int rb = tid % (KT / 4), cb = tid / (KT / 4);
-    u32x4_t v[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      int row = r0 + rb * 4 + j;
-      v[j] = row < nrows ? *(const u32x4_t*)(src + (int64_t)row * ld + cb * 8) : zero4();
-    }
-#pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      const int w = c >> 1, sh = (c & 1) * 16;
-      uint32_t e0 = (v[0][w] >> sh) & 0xffffu, e1 = (v[1][w] >> sh) & 0xffffu;
-      uint32_t e2 = (v[2][w] >> sh) & 0xffffu, e3 = (v[3][w] >> sh) & 0xffffu;
-      u32x2_t o = {e0 | (e1 << 16), e2 | (e3 << 16)};
-      *(u32x2_t*)(Xt + (cb * 8 + c) * LDT + rb * 4) = o;
-    }
-  }
+// A operand from tile rows: lane l reads row r0 + l % 32, columns
+// 16 ks + 8 (l / 32) .. +7.
+__device__ __forceinline__ bf16x8_t frag_rows(const char* tile, int r0, int ks, int lane) {
+  return *(const bf16x8_t*)(tile + toff(r0 + (lane & 31), 2 * ks + (lane >> 5)));
 }
+
+// Transposed A operand: lane l gets column col0 + l % 32 at the tile rows
+// rb + 4 hf + {0..3} and rb + 8 + 4 hf + {0..3} (hf = l / 32), which with
+// rb = row base + 16 ks is the row order of accumulator registers
+// 8 ks .. 8 ks + 7.  ds_read_b64_tr_b16 works on groups of 16 lanes: lane j
+// supplies the address of 4 consecutive 16-bit values V[j][0..3] and lane i
+// receives V[4e + i / 4][i % 4], e = 0..3; lane j points at row
+// rb + 4 hf + j / 4, columns c0 + 4 (j % 4) .. +3, so lane i receives column
+// c0 + i of those 4 rows.
+__device__ __forceinline__ bf16x8_t frag_tr(const char* tile, int col0, int rb, int lane) {
+  typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
+  const int j = lane & 15;
+  const int r = rb + 4 * (lane >> 5) + (j >> 2);
+  const int d = col0 + 16 * ((lane >> 4) & 1) + 4 * (j & 3);
+  const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      (lds_bf16x4_t*)(tile + toff(r, d >> 3) + 2 * (d & 7)));
+  const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      (lds_bf16x4_t*)(tile + toff(r + 8, d >> 3) + 2 * (d & 7)));
+  return bf16x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+}
+
+// "vmcnt = 0 and lgkmcnt = 0" (gfx9 s_waitcnt encoding).
+__device__ __forceinline__ void wait_all() { __builtin_amdgcn_s_waitcnt(0x0070); }
 
 // Write a wavefront's 32 x 64 result, held transposed in two accumulators
 // (lane = row l % 32, registers = columns), to dst rows [row0, row0 + 32)
@@ -175,10 +197,8 @@ __global__ __launch_bounds__(256) void key_extent_kernel(const uint8_t* __restri
 // Forward: wavefront = 32 queries; block = 128 queries of one (batch, head).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[KT * LD];
-  __shared__ __attribute__((aligned(16))) bf16_t Vt[HD * LDT];
-  __shared__ uint8_t ms[KT];
-  __shared__ __attribute__((aligned(16))) bf16_t stage[4][32 * LD];
+  __shared__ __attribute__((aligned(1024))) char tiles[2][2 * TILE];  // per stage: K, V
+  __shared__ __attribute__((aligned(16))) float kbias[2][KT];         // 0 or -inf per key
 
   const int bh = blockIdx.y, b = bh / a.H, j = bh % a.H;
   const int S = a.S, h = a.h;
@@ -190,7 +210,18 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
   const bf16_t* __restrict__ Vg = Qg + 2 * h;
   const uint8_t* __restrict__ mrow = a.mask + (int64_t)b * S;
   const int kend = a.kext[b];
+  const int nkb = (kend + KT - 1) / KT;
+  const __amdgpu_buffer_rsrc_t rsK = rows_rsrc(Kg, S, ld), rsV = rows_rsrc(Vg, S, ld);
+  auto bias_of = [&](int kb) {
+    const int k = kb * KT + tid;
+    return (k < kend && mrow[k] != 0) ? 0.0f : -INFINITY;
+  };
 
+  if (nkb > 0) {
+    if (tid < KT) kbias[0][tid] = bias_of(0);
+    dma_rows(rsK, 0, ld, tiles[0], wave, lane);
+    dma_rows(rsV, 0, ld, tiles[0] + TILE, wave, lane);
+  }
   // Q^T as the B operand: lane = query q0 + rr, dims 16 ks + 8 hf .. +7.
   bf16x8_t qf[4];
   {
@@ -203,26 +234,36 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
   float m = -INFINITY, lsum = 0.0f;  // running max (log2 units) and partial sum
   f32x16_t acc[2] = {zero16(), zero16()};  // O^T: dims 0-31, 32-63 x queries
 
-  for (int kb0 = 0; kb0 < kend; kb0 += KT) {
+  for (int kb = 0; kb < nkb; ++kb) {
+    const int st = kb & 1;
+    // Block kb has landed (each wavefront waits for its own loads, the
+    // barrier for everyone's) and nobody reads the other stage any more.
+    wait_all();
     __syncthreads();
-    load_rows(Kg, ld, kb0, S, Ks);
-    load_rows_t(Vg, ld, kb0, S, Vt);
-    if (tid < KT) ms[tid] = (kb0 + tid < kend) ? mrow[kb0 + tid] : 0;
-    __syncthreads();
+    float nbias = 0.0f;
+    if (kb + 1 < nkb) {
+      if (tid < KT) nbias = bias_of(kb + 1);
+      dma_rows(rsK, (kb + 1) * KT, ld, tiles[st ^ 1], wave, lane);
+      dma_rows(rsV, (kb + 1) * KT, ld, tiles[st ^ 1] + TILE, wave, lane);
+    }
+    const char* Ks = tiles[st];
+    const char* Vs = tiles[st] + TILE;
 #pragma unroll
     for (int sub = 0; sub < KT / 32; ++sub) {
-      if (kb0 + 32 * sub >= kend) break;
+      if (kb * KT + 32 * sub >= kend) break;
       // S^T (32 keys x 32 queries) = K_sub Q^T
       f32x16_t s = zero16();
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
-        s = mfma32(ld_frag(Ks + (32 * sub + rr) * LD + 16 * ks + 8 * hf), qf[ks], s);
+      for (int ks = 0; ks < 4; ++ks) s = mfma32(frag_rows(Ks, 32 * sub, ks, lane), qf[ks], s);
       float mblk = -INFINITY;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const bool valid = ms[32 * sub + acc_row(r, hf)] != 0;
-        s[r] = valid ? s[r] * a.scale_log2 : -INFINITY;
-        mblk = fmaxf(mblk, s[r]);
+      for (int g = 0; g < 4; ++g) {
+        const f32x4_t kbv = *(const f32x4_t*)&kbias[st][32 * sub + 8 * g + 4 * hf];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          s[4 * g + e] = fmaf(s[4 * g + e], a.scale_log2, kbv[e]);
+          mblk = fmaxf(mblk, s[4 * g + e]);
+        }
       }
       mblk = fmaxf(mblk, __shfl_xor(mblk, 32, 64));
       const float mnew = fmaxf(m, mblk);
@@ -246,26 +287,26 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
         const bf16x8_t pb = pack8(s, 8 * ks);
 #pragma unroll
         for (int t = 0; t < 2; ++t)
-          acc[t] = mfma32(ld_frag_t(Vt, 32 * t + rr, 32 * sub, ks, hf), pb, acc[t]);
+          acc[t] = mfma32(frag_tr(Vs, 32 * t, 32 * sub + 16 * ks, lane), pb, acc[t]);
       }
     }
+    if (kb + 1 < nkb && tid < KT) kbias[st ^ 1][tid] = nbias;
   }
   const float ltot = lsum + __shfl_xor(lsum, 32, 64);
   const float inv = ltot > 0.0f ? 1.0f / ltot : 0.0f;
   if (hf == 0 && q0 + rr < S)
     a.lse[(int64_t)bh * S + q0 + rr] = ltot > 0.0f ? m + __log2f(ltot) : 0.0f;
-  store_rows_t(acc, inv, stage[wave], a.out + (int64_t)b * S * h + j * HD, h, q0, S, nullptr);
+  __syncthreads();  // the ring becomes the output staging area
+  bf16_t* stage = (bf16_t*)&tiles[0][0] + wave * 32 * LD;
+  store_rows_t(acc, inv, stage, a.out + (int64_t)b * S * h + j * HD, h, q0, S, nullptr);
 }
 
 // ---------------------------------------------------------------------------
 // Backward, dQ: wavefront = 32 queries; loops over key blocks.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[KT * LD];
-  __shared__ __attribute__((aligned(16))) bf16_t Kt[HD * LDT];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[KT * LD];
-  __shared__ uint8_t ms[KT];
-  __shared__ __attribute__((aligned(16))) bf16_t stage[4][32 * LD];
+  __shared__ __attribute__((aligned(1024))) char tiles[2][2 * TILE];  // per stage: K, V
+  __shared__ __attribute__((aligned(16))) float kbias[2][KT];
 
   const int bh = blockIdx.y, b = bh / a.H, j = bh % a.H;
   const int S = a.S, h = a.h;
@@ -279,8 +320,19 @@ __global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
   const bf16_t* __restrict__ dOg = a.dout + (int64_t)b * S * h + j * HD;
   const uint8_t* __restrict__ mrow = a.mask + (int64_t)b * S;
   const int kend = a.kext[b];
+  const int nkb = (kend + KT - 1) / KT;
   const int q = q0 + rr;
+  const __amdgpu_buffer_rsrc_t rsK = rows_rsrc(Kg, S, ld), rsV = rows_rsrc(Vg, S, ld);
+  auto bias_of = [&](int kb) {
+    const int k = kb * KT + tid;
+    return (k < kend && mrow[k] != 0) ? 0.0f : -INFINITY;
+  };
 
+  if (nkb > 0) {
+    if (tid < KT) kbias[0][tid] = bias_of(0);
+    dma_rows(rsK, 0, ld, tiles[0], wave, lane);
+    dma_rows(rsV, 0, ld, tiles[0] + TILE, wave, lane);
+  }
   bf16x8_t qf[4], dof[4];
   float dsum = 0.0f;
 #pragma unroll
@@ -302,27 +354,37 @@ __global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
   const float lse_q = q < S ? a.lse[(int64_t)bh * S + q] : 0.0f;
 
   f32x16_t dq[2] = {zero16(), zero16()};  // dQ^T: dims x queries
-  for (int kb0 = 0; kb0 < kend; kb0 += KT) {
+  for (int kb = 0; kb < nkb; ++kb) {
+    const int st = kb & 1;
+    wait_all();
     __syncthreads();
-    load_rows(Kg, ld, kb0, S, Ks);
-    load_rows_t(Kg, ld, kb0, S, Kt);
-    load_rows(Vg, ld, kb0, S, Vs);
-    if (tid < KT) ms[tid] = (kb0 + tid < kend) ? mrow[kb0 + tid] : 0;
-    __syncthreads();
+    float nbias = 0.0f;
+    if (kb + 1 < nkb) {
+      if (tid < KT) nbias = bias_of(kb + 1);
+      dma_rows(rsK, (kb + 1) * KT, ld, tiles[st ^ 1], wave, lane);
+      dma_rows(rsV, (kb + 1) * KT, ld, tiles[st ^ 1] + TILE, wave, lane);
+    }
+    const char* Ks = tiles[st];
+    const char* Vs = tiles[st] + TILE;
 #pragma unroll
     for (int sub = 0; sub < KT / 32; ++sub) {
-      if (kb0 + 32 * sub >= kend) break;
+      if (kb * KT + 32 * sub >= kend) break;
+      // S^T = K_sub Q^T and dP^T = V_sub dO^T (keys x queries)
       f32x16_t s = zero16(), dp = zero16();
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
-        s = mfma32(ld_frag(Ks + (32 * sub + rr) * LD + 16 * ks + 8 * hf), qf[ks], s);
-        dp = mfma32(ld_frag(Vs + (32 * sub + rr) * LD + 16 * ks + 8 * hf), dof[ks], dp);
+        s = mfma32(frag_rows(Ks, 32 * sub, ks, lane), qf[ks], s);
+        dp = mfma32(frag_rows(Vs, 32 * sub, ks, lane), dof[ks], dp);
       }
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const bool valid = ms[32 * sub + acc_row(r, hf)] != 0;
-        const float p = valid ? __builtin_amdgcn_exp2f(s[r] * a.scale_log2 - lse_q) : 0.0f;
-        s[r] = p * (dp[r] - dsum);  // dS^T (unscaled)
+      for (int g = 0; g < 4; ++g) {
+        const f32x4_t kbv = *(const f32x4_t*)&kbias[st][32 * sub + 8 * g + 4 * hf];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 4 * g + e;
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, kbv[e]) - lse_q);
+          s[r] = p * (dp[r] - dsum);  // dS^T (unscaled)
+        }
       }
       // dQ^T += K^T dS^T
 #pragma unroll
@@ -330,24 +392,24 @@ __global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
         const bf16x8_t db = pack8(s, 8 * ks);
 #pragma unroll
         for (int t = 0; t < 2; ++t)
-          dq[t] = mfma32(ld_frag_t(Kt, 32 * t + rr, 32 * sub, ks, hf), db, dq[t]);
+          dq[t] = mfma32(frag_tr(Ks, 32 * t, 32 * sub + 16 * ks, lane), db, dq[t]);
       }
     }
+    if (kb + 1 < nkb && tid < KT) kbias[st ^ 1][tid] = nbias;
   }
+  __syncthreads();  // the ring becomes the output staging area
+  bf16_t* stage = (bf16_t*)&tiles[0][0] + wave * 32 * LD;
   const int nqb = (S + 31) / 32;
   float* cp = (a.colpart && q0 < S) ? a.colpart + ((int64_t)b * nqb + q0 / 32) * ld + j * HD : nullptr;
-  store_rows_t(dq, a.scale, stage[wave], a.out + (int64_t)b * S * ld + j * HD, ld, q0, S, cp);
+  store_rows_t(dq, a.scale, stage, a.out + (int64_t)b * S * ld + j * HD, ld, q0, S, cp);
 }
 
 // ---------------------------------------------------------------------------
 // Backward, dK and dV: wavefront = 32 keys; loops over query blocks.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) bf16_t Qs[KT * LD];
-  __shared__ __attribute__((aligned(16))) bf16_t Qt[HD * LDT];
-  __shared__ __attribute__((aligned(16))) bf16_t dOs[KT * LD];
-  __shared__ __attribute__((aligned(16))) bf16_t dOt[HD * LDT];
-  __shared__ float lse_s[KT], d_s[KT];
+  __shared__ __attribute__((aligned(1024))) char tiles[2][2 * TILE];  // per stage: Q, dO
+  __shared__ __attribute__((aligned(16))) float rowv[2][2][KT];       // per stage: lse, D
 
   const int bh = blockIdx.y, b = bh / a.H, j = bh % a.H;
   const int S = a.S, h = a.h;
@@ -362,7 +424,20 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
   const int key = k0 + rr;
   const bool kvalid = key < kend && a.mask[(int64_t)b * S + key] != 0;
   const bool block_live = blockIdx.x * 128 < kend;  // uniform over the block
+  const int nqb = block_live ? (S + KT - 1) / KT : 0;
+  const __amdgpu_buffer_rsrc_t rsQ = rows_rsrc(Qg, S, ld), rsD = rows_rsrc(dOg, S, h);
+  // threads 0-63 carry lse, 64-127 D of query block qb (rows past S: P = 0)
+  auto rowval = [&](int qb) {
+    const int qq = qb * KT + (tid & 63);
+    if (tid < KT) return qq < S ? a.lse[(int64_t)bh * S + qq] : INFINITY;
+    return qq < S ? a.dsum[(int64_t)bh * S + qq] : 0.0f;
+  };
 
+  if (nqb > 0) {
+    if (tid < 2 * KT) rowv[0][tid >> 6][tid & 63] = rowval(0);
+    dma_rows(rsQ, 0, ld, tiles[0], wave, lane);
+    dma_rows(rsD, 0, h, tiles[0] + TILE, wave, lane);
+  }
   bf16x8_t kf[4], vf[4];
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
@@ -376,34 +451,39 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
   }
   f32x16_t dv[2] = {zero16(), zero16()}, dk[2] = {zero16(), zero16()};  // dims x keys
 
-  for (int qb0 = 0; block_live && qb0 < S; qb0 += KT) {
+  for (int qb = 0; qb < nqb; ++qb) {
+    const int st = qb & 1;
+    wait_all();
     __syncthreads();
-    load_rows(Qg, ld, qb0, S, Qs);
-    load_rows_t(Qg, ld, qb0, S, Qt);
-    load_rows(dOg, h, qb0, S, dOs);
-    load_rows_t(dOg, h, qb0, S, dOt);
-    if (tid < KT) {
-      const int qq = qb0 + tid;
-      lse_s[tid] = qq < S ? a.lse[(int64_t)bh * S + qq] : INFINITY;
-      d_s[tid] = qq < S ? a.dsum[(int64_t)bh * S + qq] : 0.0f;
+    float nrow = 0.0f;
+    if (qb + 1 < nqb) {
+      if (tid < 2 * KT) nrow = rowval(qb + 1);
+      dma_rows(rsQ, (qb + 1) * KT, ld, tiles[st ^ 1], wave, lane);
+      dma_rows(rsD, (qb + 1) * KT, h, tiles[st ^ 1] + TILE, wave, lane);
     }
-    __syncthreads();
+    const char* Qs = tiles[st];
+    const char* dOs = tiles[st] + TILE;
 #pragma unroll
     for (int sub = 0; sub < KT / 32; ++sub) {
-      if (qb0 + 32 * sub >= S) break;
+      if (qb * KT + 32 * sub >= S) break;
       // S (32 queries x 32 keys) = Q_sub K^T;  dP = dO_sub V^T
       f32x16_t s = zero16(), dp = zero16();
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
-        s = mfma32(ld_frag(Qs + (32 * sub + rr) * LD + 16 * ks + 8 * hf), kf[ks], s);
-        dp = mfma32(ld_frag(dOs + (32 * sub + rr) * LD + 16 * ks + 8 * hf), vf[ks], dp);
+        s = mfma32(frag_rows(Qs, 32 * sub, ks, lane), kf[ks], s);
+        dp = mfma32(frag_rows(dOs, 32 * sub, ks, lane), vf[ks], dp);
       }
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int qi = 32 * sub + acc_row(r, hf);
-        const float p = kvalid ? __builtin_amdgcn_exp2f(s[r] * a.scale_log2 - lse_s[qi]) : 0.0f;
-        s[r] = p;
-        dp[r] = p * (dp[r] - d_s[qi]);  // dS (unscaled)
+      for (int g = 0; g < 4; ++g) {
+        const f32x4_t lv = *(const f32x4_t*)&rowv[st][0][32 * sub + 8 * g + 4 * hf];
+        const f32x4_t dv4 = *(const f32x4_t*)&rowv[st][1][32 * sub + 8 * g + 4 * hf];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 4 * g + e;
+          const float p = kvalid ? __builtin_amdgcn_exp2f(s[r] * a.scale_log2 - lv[e]) : 0.0f;
+          s[r] = p;
+          dp[r] = p * (dp[r] - dv4[e]);  // dS (unscaled)
+        }
       }
       // dV^T += dO^T P;  dK^T += Q^T dS
 #pragma unroll
@@ -412,18 +492,18 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
         const bf16x8_t db = pack8(dp, 8 * ks);
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-          dv[t] = mfma32(ld_frag_t(dOt, 32 * t + rr, 32 * sub, ks, hf), pb, dv[t]);
-          dk[t] = mfma32(ld_frag_t(Qt, 32 * t + rr, 32 * sub, ks, hf), db, dk[t]);
+          dv[t] = mfma32(frag_tr(dOs, 32 * t, 32 * sub + 16 * ks, lane), pb, dv[t]);
+          dk[t] = mfma32(frag_tr(Qs, 32 * t, 32 * sub + 16 * ks, lane), db, dk[t]);
         }
       }
     }
+    if (qb + 1 < nqb && tid < 2 * KT) rowv[st ^ 1][tid >> 6][tid & 63] = nrow;
   }
-  __syncthreads();
-  // Stage the outputs through the (now free) Q tiles: 4 waves x 32 x LD.
-  bf16_t* stage = (wave < 2 ? Qs : dOs) + (wave & 1) * 32 * LD;
+  __syncthreads();  // the ring becomes the output staging area
+  bf16_t* stage = (bf16_t*)&tiles[0][0] + wave * 32 * LD;
   bf16_t* dst = a.out + (int64_t)b * S * ld + j * HD;
-  const int nqb = (S + 31) / 32;
-  float* cp = (a.colpart && k0 < S) ? a.colpart + ((int64_t)b * nqb + k0 / 32) * ld + j * HD : nullptr;
+  const int nkb32 = (S + 31) / 32;
+  float* cp = (a.colpart && k0 < S) ? a.colpart + ((int64_t)b * nkb32 + k0 / 32) * ld + j * HD : nullptr;
   store_rows_t(dk, a.scale, stage, dst + h, ld, k0, S, cp ? cp + h : nullptr);
   __builtin_amdgcn_wave_barrier();
   store_rows_t(dv, 1.0f, stage, dst + 2 * h, ld, k0, S, cp ? cp + 2 * h : nullptr);
