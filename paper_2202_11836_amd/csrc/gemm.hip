@@ -1,12 +1,13 @@
 // Dense contractions of the encoder layer: bf16 MFMA GEMM (fp32 accumulate)
 // and an fp32 vector-ALU GEMM, both with fused epilogues.
 //
-// bf16 path: 256 threads = 4 wavefronts in a 2 x 2 grid; each wavefront owns
-// a (BM/2) x (BN/2) sub-tile computed with v_mfma_f32_32x32x16_bf16.  k-tiles
-// of 64 go straight from HBM into a 2-stage LDS ring with direct-to-LDS
-// buffer loads, issued a k-tile and a k-step ahead, so no staging registers
-// and no LDS store instructions sit in the main loop, and the one barrier per
-// k-tile overlaps the MFMAs of the last k-step.  Operands stored m/n-contiguous in
+// bf16 path: a persistent work-group per CU walks BM x BN output tiles; its
+// wavefronts (8 for 256 x 256 tiles, two per SIMD; 4 otherwise) form a
+// 2 x (waves / 2) grid, each owning a sub-tile computed with
+// v_mfma_f32_32x32x16_bf16.  k-tiles of 64 go straight from HBM into a ring
+// of LDS slots with direct-to-LDS buffer loads, issued ahead of use, so no
+// staging registers and no LDS store instructions sit in the main loop, and
+// the one barrier per k-tile overlaps the MFMAs of the last k-step.  Operands stored m/n-contiguous in
 // HBM keep that layout in LDS and their MFMA fragments are read with gfx950's
 // transposing LDS read.
 #include <algorithm>
@@ -67,14 +68,13 @@ __device__ __forceinline__ int64_t batch_off(int zb, int zdiv, int64_t s1, int64
 // ---------------------------------------------------------------------------
 // bf16 MFMA GEMM
 //
-// Block = 4 wavefronts in a 2 x 2 grid over a BM x BN tile; each wavefront
-// owns (BM/2) x (BN/2) = TM x TN accumulators of 32 x 32.  k-tiles of 64 are
-// double-buffered in LDS (up to 147 KB of gfx950's 160 KB per CU): the next tile is fetched into registers while the
-// current one feeds the MFMAs, then written to the other LDS buffer, so one
-// barrier per k-tile suffices.  The epilogue stages each 32-row slab of a
-// wavefront's accumulators through LDS (fp32) so that bias / activation /
-// residual operands are read and the results written as 16-byte row
-// segments.
+// Block = 2 x (waves / 2) wavefronts over a BM x BN tile; each wavefront
+// owns a (BM/2) x (BN/(waves/2)) sub-tile = TM x TN accumulators of 32 x 32.
+// k-tiles of 64 sit in a ring of NS LDS slots (with the epilogue staging
+// area, up to the full 160 KB of a gfx950 CU), one barrier per k-tile.  The
+// epilogue stages each 16-row half of a wavefront's 32-row slab through LDS
+// (fp32) so that bias / activation / residual operands are read and the
+// results written as 16-byte row segments.
 // ---------------------------------------------------------------------------
 // k-tile depth and ring depth per tile shape: a ring of NS k-tiles of BK
 // keeps NS - 1 k-tiles in flight behind the one being consumed.
@@ -84,24 +84,33 @@ template <int BM, int BN>
 struct RingShape {
   static constexpr int BK = 64;
   static constexpr int NS = (BM == 256 && BN == 256) ? 2 : (BM == 256 ? 3 : 4);
+  // Wavefronts per work-group: 2 along m times WAVES / 2 along n.  The
+  // 256 x 256 tile runs 8 (two per SIMD, 128 x 64 each): while one
+  // wavefront waits on loads, a barrier or its epilogue, the other's MFMAs
+  // keep the matrix core busy.
+  static constexpr int WAVES = (BM == 256 && BN == 256) ? 8 : 4;
 };
 
 template <int BM, int BN, bool AK, bool BKM>
 struct TileCfg {
   static constexpr int BK = RingShape<BM, BN>::BK;
   static constexpr int NS = RingShape<BM, BN>::NS;
-  static constexpr int WM = BM / 2, WN = BN / 2;
+  static constexpr int WAVES = RingShape<BM, BN>::WAVES;
+  static constexpr int WGN = WAVES / 2;
+  static constexpr int THREADS = 64 * WAVES;
+  static constexpr int WM = BM / 2, WN = BN / WGN;
   static constexpr int TM = WM / 32, TN = WN / 32;
   static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
   static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
   // direct-to-LDS load instructions per k-tile per wavefront (1 KB each)
-  static constexpr int DMA_PER_TILE = STAGE_BYTES / 1024 / 4;
+  static constexpr int DMA_PER_TILE = STAGE_BYTES / 1024 / WAVES;
   // Epilogue staging, beside the ring: 16 rows x WN fp32 per wavefront.
-  static constexpr int EPI_BYTES = 4 * 16 * WN * 4;
+  static constexpr int EPI_BYTES = WAVES * 16 * WN * 4;
   static constexpr int LDS_BYTES = NS * STAGE_BYTES + EPI_BYTES;
   static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
   static_assert((NS - 2) * DMA_PER_TILE <= 63, "vmcnt range");
-  static_assert(STAGE_BYTES % 4096 == 0, "whole 1 KB blocks per wavefront");
+  static_assert(A_BYTES % (1024 * WAVES) == 0 && B_BYTES % (1024 * WAVES) == 0,
+                "whole 1 KB blocks per wavefront");
 };
 
 // Buffer resource over [base, base + bytes): loads past the end return 0.
@@ -132,13 +141,13 @@ __device__ __forceinline__ int kswz(int r) {
   return BK == 64 ? ((r >> 1) & 7) : ((r >> 2) & 3);
 }
 
-template <int R, bool KMAJ, int BK>
+template <int R, bool KMAJ, int BK, int W>
 __device__ __forceinline__ void dma_tile(__amdgpu_buffer_rsrc_t rs, int64_t ld, int k0, char* dst,
                                          int wave, int lane) {
   constexpr int NB = R * BK * 2 / 1024;  // 1 KB blocks in the tile
 #pragma unroll
-  for (int i = 0; i < NB / 4; ++i) {
-    const int q = wave * (NB / 4) + i;
+  for (int i = 0; i < NB / W; ++i) {
+    const int q = wave * (NB / W) + i;
     int64_t elem;
     if constexpr (KMAJ) {
       constexpr int CPR = BK / 8;   // chunks per row
@@ -321,8 +330,8 @@ __device__ __forceinline__ void issue_ktile(const GemmArgs& g, const TileOps& T,
                                             int wave, int lane) {
   using C = TileCfg<BM, BN, AK, BKM>;
   char* b = smem + (t % C::NS) * C::STAGE_BYTES;
-  dma_tile<BM, AK, C::BK>(T.rsA, g.lda, T.kA0 + t * C::BK, b, wave, lane);
-  dma_tile<BN, BKM, C::BK>(T.rsB, g.ldb, T.kB0 + t * C::BK, b + C::A_BYTES, wave, lane);
+  dma_tile<BM, AK, C::BK, C::WAVES>(T.rsA, g.lda, T.kA0 + t * C::BK, b, wave, lane);
+  dma_tile<BN, BKM, C::BK, C::WAVES>(T.rsB, g.ldb, T.kB0 + t * C::BK, b + C::A_BYTES, wave, lane);
 }
 
 // s_waitcnt immediate (gfx9 encoding: vmcnt[3:0] | expcnt[6:4] |
@@ -349,7 +358,7 @@ __device__ __forceinline__ void wait_ktile(int after) {
 // + gridDim.x, ...  The first NS k-tiles of the next output tile are
 // loaded while the current tile's epilogue runs.
 template <int BM, int BN, bool AK, bool BKM, int EPI, bool OUTF32>
-__global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
+__global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_kernel(GemmArgs g) {
   using C = TileCfg<BM, BN, AK, BKM>;
   constexpr int TM = C::TM, TN = C::TN, NS = C::NS;
   __shared__ __attribute__((aligned(1024))) char smem[C::LDS_BYTES];
@@ -357,7 +366,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
   const int nbm = (g.M + BM - 1) / BM, nbn = (g.N + BN - 1) / BN;
   const int total = nbm * nbn * g.zdiv_total;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
   const int hf = lane >> 5, rr = lane & 31;
   constexpr int KS = C::BK / 16;
 
@@ -478,7 +487,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
     float* stg = (float*)(smem + NS * C::STAGE_BYTES) + wave * 16 * C::WN;
     // Optional column sums (EPI_MUL): every lane keeps one 8-column chunk
     // (CH divides 64) over the rows it writes.
-    constexpr bool COLSUM = EPI == EPI_MUL && CH == 16 && C::WM == 128;
+    constexpr bool COLSUM = EPI == EPI_MUL && (CH == 16 || CH == 8) && C::WM == 128;
     float csum[8] = {0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
@@ -526,11 +535,11 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs g) {
       // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same columns: fixed-order sum
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        csum[e] += __shfl_xor(csum[e], 16, 64);
-        csum[e] += __shfl_xor(csum[e], 32, 64);
+#pragma unroll
+        for (int o = CH; o < 64; o <<= 1) csum[e] += __shfl_xor(csum[e], o, 64);
       }
-      const int n = nw + (lane & 15) * 8;
-      if (lane < 16 && n < g.N) {
+      const int n = nw + (lane % CH) * 8;
+      if (lane < CH && n < g.N) {
         float* P = g.colpart + (int64_t)(mw / C::WM) * g.N + n;
         *(f32x4_t*)P = f32x4_t{csum[0], csum[1], csum[2], csum[3]};
         *(f32x4_t*)(P + 4) = f32x4_t{csum[4], csum[5], csum[6], csum[7]};
@@ -656,7 +665,7 @@ hipError_t launch_bf16(const GemmArgs& g0, int batch, hipStream_t st) {
   int64_t grid = std::min<int64_t>(total, device_cus());
   if (grid >= 8) grid -= grid % 8;
   hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, AK, BKM, EPI, OUTF32>), dim3((unsigned)grid),
-                     dim3(NT), 0, st, g);
+                     dim3(TileCfg<BM, BN, AK, BKM>::THREADS), 0, st, g);
   return hipGetLastError();
 }
 
