@@ -231,7 +231,7 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
       qf[ks] = q < S ? ld_frag(Qg + (int64_t)q * ld + 16 * ks + 8 * hf)
                      : __builtin_bit_cast(bf16x8_t, zero4());
   }
-  float m = -INFINITY, lsum = 0.0f;  // running max (log2 units) and partial sum
+  float m = -INFINITY, lsum = 0.0f;  // exponent offset (log2 units) and partial sum
   f32x16_t acc[2] = {zero16(), zero16()};  // O^T: dims 0-31, 32-63 x queries
 
   for (int kb = 0; kb < nkb; ++kb) {
@@ -266,21 +266,28 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
         }
       }
       mblk = fmaxf(mblk, __shfl_xor(mblk, 32, 64));
-      const float mnew = fmaxf(m, mblk);
-      const float off = mnew == -INFINITY ? 0.0f : mnew;
-      const float alpha = __builtin_amdgcn_exp2f(m - off);
+      // The exponent offset m moves only when a block maximum exceeds it by
+      // more than 8 (log2 units), so exp2(s - m) <= 256 and most blocks
+      // skip rescaling the output accumulators (a wavefront-uniform test).
+      const bool grow = mblk > m + 8.0f;
+      if (__any(grow)) {
+        const float mn = grow ? mblk : m;
+        const float alpha = __builtin_amdgcn_exp2f(m - (mn == -INFINITY ? 0.0f : mn));
+        lsum *= alpha;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[t][r] *= alpha;
+        m = mn;
+      }
+      const float off = m == -INFINITY ? 0.0f : m;
       float ps = 0.0f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         s[r] = __builtin_amdgcn_exp2f(s[r] - off);
         ps += s[r];
       }
-      lsum = lsum * alpha + ps;
-      m = mnew;
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[t][r] *= alpha;
+      lsum += ps;
       // O^T += V_sub^T P^T
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
