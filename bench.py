@@ -109,6 +109,70 @@ def cpu_baseline(cfg, budget_s: float = 10.0):
                       f"fwd+bwd, fp64 numpy ({dt:.1f} s)"}
 
 
+def depth_sweep(cfg, depths, steps, warmup):
+    """Per-layer forward+backward time of cfg at several depths L, and the
+    least-squares line t(L) = a L + b over them: the allocator models a
+    device's time for a contiguous block of layers as the sum of per-layer
+    costs plus a constant (section III-A), which holds when the fit is
+    tight and b is small."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2202_11836_amd import Stage
+
+    inp = synth.make_inputs(cfg)
+    dtype = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    x = torch.from_numpy(inp["x"].astype(np.float32)).to(dtype).cuda()
+    dy = torch.from_numpy(inp["dy"].astype(np.float32)).to(dtype).cuda()
+    mask = torch.from_numpy(inp["mask"]).cuda()
+    rows = []
+    for L in depths:
+        st = Stage(L, cfg.hidden, cfg.heads, cfg.ffn, seed=cfg.seed, dtype=cfg.dtype)
+        y = torch.empty_like(x)
+        dx = torch.empty_like(x)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        for _ in range(warmup):
+            st.forward(x, mask, out=y)
+            st.backward(dy, out=dx)
+        torch.cuda.synchronize()
+        fwd = bwd = 0.0
+        for _ in range(steps):
+            ev[0].record()
+            st.forward(x, mask, out=y)
+            ev[1].record()
+            st.backward(dy, out=dx)
+            ev[2].record()
+            torch.cuda.synchronize()
+            fwd += ev[0].elapsed_time(ev[1]) / steps
+            bwd += ev[1].elapsed_time(ev[2]) / steps
+        st.close()
+        rows.append({"L": L, "fwd_ms": fwd, "bwd_ms": bwd, "step_ms": fwd + bwd,
+                     "per_layer_ms": (fwd + bwd) / L})
+        print(f"L={L:3d}  step {fwd + bwd:8.3f} ms  per layer {(fwd + bwd) / L:7.3f} ms",
+              file=sys.stderr, flush=True)
+    Ls = np.array([r["L"] for r in rows], dtype=np.float64)
+    ts = np.array([r["step_ms"] for r in rows])
+    a, b = np.polyfit(Ls, ts, 1) if len(rows) > 1 else (ts[0] / Ls[0], 0.0)
+    pred = a * Ls + b
+    ss = float(((ts - ts.mean()) ** 2).sum())
+    r2 = 1.0 - float(((ts - pred) ** 2).sum()) / ss if ss > 0 else 1.0
+    return {
+        "metric": "per-layer fwd+bwd time vs stage depth on 1 MI355X",
+        "unit": "ms",
+        "higher_is_better": False,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded N(0,1) inputs, N(0,0.02) weights)",
+        "steps": steps,
+        "warmup": warmup,
+        "config": {"workload": f"{cfg.name}: h{cfg.hidden}, {cfg.heads} heads, ffn {cfg.ffn}, "
+                               f"B{cfg.batch} x S{cfg.seq}, valid lengths in "
+                               f"[{cfg.len_lo},{cfg.len_hi}]"},
+        "sweep": rows,
+        "fit": {"ms_per_layer": float(a), "ms_constant": float(b), "r2": r2},
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -120,6 +184,10 @@ def main():
     ap.add_argument("--breakdown", action="store_true", help="per-site times to stderr")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
+    ap.add_argument("--sweep-layers", default=None,
+                    help="comma-separated depths: time --config at each depth and report the "
+                         "per-layer fwd+bwd time and a linear fit of step time against depth "
+                         "(the per-layer cost model of the layer allocator, section III-A)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="after timing, copy a fresh buffer of this size once (the known-size "
                          "copy that scales rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -137,6 +205,11 @@ def main():
     from paper_2202_11836_amd import Stage, stage_site_count, stage_site_name
 
     cfg = synth.CONFIGS[args.config]
+    if args.sweep_layers:
+        torch.cuda.set_device(0)
+        print(json.dumps(depth_sweep(cfg, [int(v) for v in args.sweep_layers.split(",")],
+                                     args.steps, args.warmup)), flush=True)
+        return
     if args.layers is not None:
         cfg = cfg.with_(L=args.layers)
     torch.cuda.set_device(0)
