@@ -113,7 +113,7 @@ def depth_sweep(cfg, depths, steps, warmup):
     """Per-layer forward+backward time of cfg at several depths L, and the
     least-squares line t(L) = a L + b over them: the allocator models a
     device's time for a contiguous block of layers as the sum of per-layer
-    costs plus a constant (section III-A), which holds when the fit is
+    costs plus a constant (section IV-C), which holds when the fit is
     tight and b is small."""
     import numpy as np
     import torch
@@ -187,7 +187,7 @@ def main():
     ap.add_argument("--sweep-layers", default=None,
                     help="comma-separated depths: time --config at each depth and report the "
                          "per-layer fwd+bwd time and a linear fit of step time against depth "
-                         "(the per-layer cost model of the layer allocator, section III-A)")
+                         "(the per-layer cost model of the layer allocator, section IV-C)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="after timing, copy a fresh buffer of this size once (the known-size "
                          "copy that scales rocprofv3 FETCH_SIZE / WRITE_SIZE)")
