@@ -1,4 +1,5 @@
-"""Thin ctypes binding of the encoder-stage C ABI (include/stage.h).
+"""Thin ctypes binding of the C ABI of libskystage.so: the encoder stage
+(include/stage.h) and the host-side layer allocator (include/alloc.h).
 
 Argument marshalling only: torch tensors supply device memory and the HIP
 stream (torch.cuda.current_stream()); every step of the stage runs in the
@@ -22,13 +23,24 @@ SAVED_NAMES = ("X", "QKV", "CTX", "H1", "GD", "G")  # GD = GELU'(U)
 KIND_PARAM, KIND_GRAD, KIND_SAVED = 0, 1, 2
 STATUS_NAMES = {0: "OK", 1: "EINVAL", 2: "ESTATE", 3: "ENOMEM", 4: "EHIP"}
 
-EXPORTED = ("stage_init", "stage_set_stream", "stage_forward", "stage_backward", "stage_param",
+ALLOC_OK, ALLOC_EINVAL, ALLOC_ENOFIT = range(3)
+ALLOC_CT_PER_LAYER, ALLOC_CT_PER_DEVICE = 0, 1
+ALLOC_STATUS_NAMES = {0: "OK", 1: "EINVAL", 2: "ENOFIT"}
+
+EXPORTED = ("alloc_coarse", "alloc_fine", "alloc_workloads", "stage_init", "stage_set_stream", "stage_forward", "stage_backward", "stage_param",
             "stage_grad", "stage_set_param", "stage_read", "stage_tensor_bytes",
             "stage_trace_site", "stage_trace_mask", "stage_trace_read", "stage_site_count",
             "stage_site_name",
             "stage_last_error", "stage_destroy")
 
 _lib = None
+
+
+class AllocError(RuntimeError):
+    def __init__(self, status: int, pi=None):
+        super().__init__(ALLOC_STATUS_NAMES.get(status, str(status)))
+        self.status = status
+        self.pi = pi  # last partition index (ENOFIT)
 
 
 class StageError(RuntimeError):
@@ -82,6 +94,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.stage_last_error.restype = ctypes.c_char_p
     lib.stage_destroy.argtypes = [vp]
     lib.stage_destroy.restype = None
+    dp, ip = ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)
+    lib.alloc_coarse.argtypes = [i32, i32, dp, dp, ip, ip]
+    lib.alloc_coarse.restype = i32
+    lib.alloc_fine.argtypes = [i32, i32, dp, dp, dp, dp, dp, i32, ip, ip]
+    lib.alloc_fine.restype = i32
+    lib.alloc_workloads.argtypes = [i32, i32, dp, dp, dp, ip, i32, dp]
+    lib.alloc_workloads.restype = i32
     _lib = lib
     return lib
 
@@ -295,3 +314,61 @@ class Stage:
             self.close()
         except Exception:
             pass
+
+
+# ---------------------------------------------------------------------------
+# Layer allocator (host code; include/alloc.h)
+# ---------------------------------------------------------------------------
+def _dvec(v):
+    v = [float(x) for x in v]
+    return (ctypes.c_double * max(len(v), 1))(*v), len(v)
+
+
+def _ivec(v, n=None):
+    v = [int(x) for x in v] if v is not None else [0] * n
+    return (ctypes.c_int * max(len(v), 1))(*v)
+
+
+def alloc_coarse(lm, dm):
+    """Algorithm 1: returns (pi, sweeps); raises AllocError (with .pi, the
+    last partition index, for ENOFIT)."""
+    a_lm, L = _dvec(lm)
+    a_dm, D = _dvec(dm)
+    pi = _ivec(None, D + 1)
+    n = ctypes.c_int(0)
+    st = load_library().alloc_coarse(L, D, a_lm, a_dm, pi, ctypes.byref(n))
+    if st != ALLOC_OK:
+        raise AllocError(st, list(pi) if st == ALLOC_ENOFIT else None)
+    return list(pi), n.value
+
+
+def alloc_fine(dt, dm, ct, lf, lm, pi, max_iter: int):
+    """Algorithm 2 from partition pi: returns (tuned pi, rounds)."""
+    a_dt, D = _dvec(dt)
+    a_dm, _ = _dvec(dm)
+    a_ct, _ = _dvec(ct)
+    a_lf, L = _dvec(lf)
+    a_lm, _ = _dvec(lm)
+    p = _ivec(pi)
+    if len(pi) != D + 1 or len(dm) != D or len(ct) != D or len(lm) != L:
+        raise AllocError(ALLOC_EINVAL)
+    n = ctypes.c_int(0)
+    st = load_library().alloc_fine(L, D, a_dt, a_dm, a_ct, a_lf, a_lm, int(max_iter), p,
+                                   ctypes.byref(n))
+    if st != ALLOC_OK:
+        raise AllocError(st)
+    return list(p), n.value
+
+
+def alloc_workloads(dt, ct, lf, pi, mode: int = ALLOC_CT_PER_LAYER):
+    """Workload of every device under partition pi."""
+    a_dt, D = _dvec(dt)
+    a_ct, _ = _dvec(ct)
+    a_lf, L = _dvec(lf)
+    if len(pi) != D + 1 or len(ct) != D:
+        raise AllocError(ALLOC_EINVAL)
+    out = (ctypes.c_double * D)()
+    st = load_library().alloc_workloads(L, D, a_dt, a_ct, a_lf, _ivec(pi), int(mode), out)
+    if st != ALLOC_OK:
+        raise AllocError(st)
+    return list(out)

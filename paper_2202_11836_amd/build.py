@@ -1,6 +1,7 @@
 """Build the HIP encoder-stage library (gfx950) in-tree.
 
-Compiles every ``csrc/*.hip`` with hipcc for gfx950 and links them into
+Compiles every ``csrc/*.hip`` with hipcc for gfx950 (and the host-only
+``csrc/*.cpp``) and links them into
 ``paper_2202_11836_amd/libskystage.so``.  Always recompiles (the caller asks
 for a fresh build); sources compile in parallel.
 """
@@ -29,12 +30,17 @@ COMMON_FLAGS = [
 
 
 def _sources():
-    return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
+    return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC)
+                  if f.endswith(".hip") or f.endswith(".cpp"))
 
 
 def _compile(src: str) -> str:
-    obj = os.path.join(BUILD_DIR, os.path.basename(src)[:-4] + ".o")
-    cmd = [HIPCC] + COMMON_FLAGS + ["-c", src, "-o", obj]
+    base, ext = os.path.splitext(os.path.basename(src))
+    obj = os.path.join(BUILD_DIR, base + ext.replace(".", "_") + ".o")
+    if ext == ".cpp":  # host-only code
+        cmd = [HIPCC, "-O3", "-std=c++17", "-fPIC", "-c", src, "-o", obj]
+    else:
+        cmd = [HIPCC] + COMMON_FLAGS + ["-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")

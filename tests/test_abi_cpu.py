@@ -1,6 +1,6 @@
 """CPU-side checks of the boundary: the built library loads without a GPU and
-exports every function include/stage.h declares; the binding declares the
-same set; no product module imports the oracle."""
+exports every function include/*.h declares; the binding declares the same
+set; no product module imports the oracle."""
 import ctypes
 import os
 import re
@@ -8,20 +8,23 @@ import re
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "stage.h")
+HEADERS = [os.path.join(ROOT, "include", f) for f in sorted(os.listdir(os.path.join(ROOT, "include")))
+           if f.endswith(".h")]
 LIB = os.path.join(ROOT, "paper_2202_11836_amd", "libskystage.so")
 
 
 def declared_functions():
-    src = open(HEADER).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(stage_[a-z_]+)\s*\(", src)))
+    names = set()
+    for h in HEADERS:
+        src = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b((?:stage|alloc)_[a-z_]+)\s*\(", src))
+    return sorted(names)
 
 
 def test_header_declares_the_stage_calls():
     names = declared_functions()
     for n in ("stage_init", "stage_forward", "stage_backward", "stage_param", "stage_grad",
-              "stage_destroy", "stage_last_error"):
+              "stage_destroy", "stage_last_error", "alloc_coarse", "alloc_fine", "alloc_workloads"):
         assert n in names
 
 
