@@ -167,33 +167,63 @@ __device__ __forceinline__ void dma_tile(__amdgpu_buffer_rsrc_t rs, int64_t ld, 
   }
 }
 
-// MFMA operand fragment: 8 consecutive k (offset ks * 16 + 8 * (lane / 32)) of
-// row r0 + lane % 32.  k-major: one 16-byte read.  m/n-major: two
+// MFMA operand fragments: 8 consecutive k (offset ks * 16 + 8 * (lane / 32))
+// of row r0 + lane % 32.  k-major: one 16-byte read.  m/n-major: two
 // ds_read_b64_tr_b16.  That instruction works on groups of 16 lanes: lane j
 // supplies the address of 4 consecutive 16-bit values V[j][0..3], and lane i
 // receives V[4e + i / 4][i % 4] for e = 0..3.  Lane j of a group points at
 // k-row k0 + j / 4, columns mb + 4 (j % 4), so lane i receives column mb + i
 // at k-rows k0 .. k0 + 3 (the second read: k0 + 4 .. k0 + 7).
-template <int R, bool KMAJ, int BK>
-__device__ __forceinline__ bf16x8_t frag(const char* S, int r0, int ks, int lane) {
-  if constexpr (KMAJ) {
-    const int r = r0 + (lane & 31);
-    const int c = 2 * ks + (lane >> 5);
-    return *(const bf16x8_t*)(S + r * (2 * BK) + 16 * (c ^ kswz<BK>(r)));
-  } else {
-    typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
-    const int grp = lane >> 4, j = lane & 15;
-    const int kr = ks * 16 + 8 * (grp >> 1) + (j >> 2);
-    const int col = r0 + 16 * (grp & 1) + 4 * (j & 3);
-    const int off = 16 * ((col >> 3) ^ (4 * (kr & 3))) + 2 * (col & 7);
-    const char* p = S + kr * (2 * R) + off;
-    const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-        (__attribute__((address_space(3))) bf16x4_t*)(p));
-    const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-        (__attribute__((address_space(3))) bf16x4_t*)(p + 4 * (2 * R)));
-    return bf16x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+typedef __attribute__((address_space(3))) char lds_char_t;
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+
+// Per-lane LDS addresses of one operand's fragments in ring slot 0, so that
+// every fragment read in the main loop is one instruction with an immediate
+// offset (no per-read address arithmetic).  k-major: one address per
+// k-step, fragment f (32 rows further) at +f * 32 * 2 BK.  m/n-major: one
+// address per fragment, k-step ks at +ks * 16 * 2R, the second transposing
+// read at +4 * 2R.  (The swizzle terms depend only on the lane because the
+// wavefront's first row is a multiple of 32.)
+template <int R, bool KMAJ, int BK, int NF>
+struct FragPtrs {
+  static constexpr int KS = BK / 16;
+  static constexpr int N = KMAJ ? KS : NF;
+  uint32_t p[N];
+  __device__ __forceinline__ void init(uint32_t base, int r0, int lane) {
+    if constexpr (KMAJ) {
+      const int r = r0 + (lane & 31);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        p[ks] = base + r * (2 * BK) + 16 * ((2 * ks + (lane >> 5)) ^ kswz<BK>(r));
+    } else {
+      const int grp = lane >> 4, j = lane & 15;
+      const int kr = 8 * (grp >> 1) + (j >> 2);
+#pragma unroll
+      for (int f = 0; f < NF; ++f) {
+        const int col = r0 + f * 32 + 16 * (grp & 1) + 4 * (j & 3);
+        p[f] = base + kr * (2 * R) + 16 * ((col >> 3) ^ (4 * (kr & 3))) + 2 * (col & 7);
+      }
+    }
   }
-}
+  __device__ __forceinline__ void advance(int delta) {
+#pragma unroll
+    for (int n = 0; n < N; ++n) p[n] += delta;
+  }
+  // fragment f of k-step ks
+  __device__ __forceinline__ bf16x8_t get(int f, int ks) const {
+    if constexpr (KMAJ) {
+      return *(const __attribute__((address_space(3))) bf16x8_t*)(
+          (const lds_char_t*)(uintptr_t)p[ks] + f * 32 * (2 * BK));
+    } else {
+      const lds_char_t* q = (const lds_char_t*)(uintptr_t)p[f] + ks * 16 * (2 * R);
+      const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+          (__attribute__((address_space(3))) bf16x4_t*)(q));
+      const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+          (__attribute__((address_space(3))) bf16x4_t*)(q + 4 * (2 * R)));
+      return bf16x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    }
+  }
+};
 
 __device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
   return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)a) |
@@ -365,7 +395,8 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
 
   const int nbm = (g.M + BM - 1) / BM, nbn = (g.N + BN - 1) / BN;
   const int total = nbm * nbn * g.zdiv_total;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS DMA targets in SGPRs
   const int wm = wave / C::WGN, wn = wave % C::WGN;
   const int hf = lane >> 5, rr = lane & 31;
   constexpr int KS = C::BK / 16;
@@ -391,14 +422,18 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
     // The first k-tiles are in flight (issued before the previous epilogue
     // or above); wait for everything outstanding, then read k-tile 0.
     bf16x8_t af[2][TM], bfr[2][TN];
+    FragPtrs<BM, AK, C::BK, TM> pa;
+    FragPtrs<BN, BKM, C::BK, TN> pb;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_char_t*)smem;
+    pa.init(lds0, wm * C::WM, lane);
+    pb.init(lds0 + C::A_BYTES, wn * C::WN, lane);
     wait_vm_lgkm0<0>();
     __syncthreads();
     if (ntiles > 0) {
 #pragma unroll
-      for (int i = 0; i < TM; ++i) af[0][i] = frag<BM, AK, C::BK>(smem, wm * C::WM + i * 32, 0, lane);
+      for (int i = 0; i < TM; ++i) af[0][i] = pa.get(i, 0);
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
-        bfr[0][j] = frag<BN, BKM, C::BK>(smem + C::A_BYTES, wn * C::WN + j * 32, 0, lane);
+      for (int j = 0; j < TN; ++j) bfr[0][j] = pb.get(j, 0);
     }
     // Main loop.  While the MFMAs of k-step ks run, the fragments of ks + 1
     // are read; in the last k-step of a k-tile they come from the next
@@ -407,29 +442,26 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
     // landed and nobody reads k-tile t's slot any more), refill that slot
     // with k-tile t + NS, then read.
     for (int t = 0; t < ntiles; ++t) {
-      const char* As = smem + (t % NS) * C::STAGE_BYTES;
-      const char* Bs = As + C::A_BYTES;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         const int cur = ks & 1, nxt = cur ^ 1;
         if (ks + 1 < KS) {
 #pragma unroll
-          for (int i = 0; i < TM; ++i)
-            af[nxt][i] = frag<BM, AK, C::BK>(As, wm * C::WM + i * 32, ks + 1, lane);
+          for (int i = 0; i < TM; ++i) af[nxt][i] = pa.get(i, ks + 1);
 #pragma unroll
-          for (int j = 0; j < TN; ++j)
-            bfr[nxt][j] = frag<BN, BKM, C::BK>(Bs, wn * C::WN + j * 32, ks + 1, lane);
+          for (int j = 0; j < TN; ++j) bfr[nxt][j] = pb.get(j, ks + 1);
         } else if (t + 1 < ntiles) {
           wait_ktile<C::DMA_PER_TILE, NS>(min(ntiles - 1, t + NS - 1) - (t + 1));
           __syncthreads();
           if (t + NS < ntiles) issue_ktile<BM, BN, AK, BKM>(g, T, t + NS, smem, wave, lane);
-          const char* An = smem + ((t + 1) % NS) * C::STAGE_BYTES;
+          // move the fragment pointers to the next ring slot
+          const int delta = ((t + 1) % NS == 0) ? -(NS - 1) * C::STAGE_BYTES : C::STAGE_BYTES;
+          pa.advance(delta);
+          pb.advance(delta);
 #pragma unroll
-          for (int i = 0; i < TM; ++i)
-            af[nxt][i] = frag<BM, AK, C::BK>(An, wm * C::WM + i * 32, 0, lane);
+          for (int i = 0; i < TM; ++i) af[nxt][i] = pa.get(i, 0);
 #pragma unroll
-          for (int j = 0; j < TN; ++j)
-            bfr[nxt][j] = frag<BN, BKM, C::BK>(An + C::A_BYTES, wn * C::WN + j * 32, 0, lane);
+          for (int j = 0; j < TN; ++j) bfr[nxt][j] = pb.get(j, 0);
         }
         // Keep the scheduler from sinking the fragment reads down to their
         // uses: they must be in flight while these MFMAs execute.
