@@ -115,6 +115,21 @@ stage_status stage_forward(stage_t* s, const void* x, const uint8_t* key_mask, i
  */
 stage_status stage_backward(stage_t* s, const void* dy, void* dx);
 
+/*
+ * Device memory.  stage_device_bytes: bytes the library holds for s
+ * (parameters, gradients, the saved-activation record and the workspace, as
+ * requested from hipMalloc).  stage_memory_model: the same figure predicted
+ * without a device for a stage of these dims after a forward of batch x seq
+ * tokens, split into per_layer (one layer's parameters, gradients and saved
+ * activations: the layer memory lm that the allocator's benchmark stage
+ * measures, section IV-B) and shared (workspace held once per stage), so
+ * that a stage of L layers holds L * per_layer + shared.  EINVAL for dims
+ * stage_init rejects or negative batch / seq.  Host arithmetic only.
+ */
+stage_status stage_device_bytes(const stage_t* s, int64_t* bytes);
+stage_status stage_memory_model(int hidden, int heads, int ffn, int batch, int seq,
+                                stage_dtype dtype, int64_t* per_layer, int64_t* shared);
+
 /* Device pointer, element count and dtype of parameter `which` of `layer`. */
 stage_status stage_param(stage_t* s, int layer, int which, void** dev_ptr, int64_t* numel,
                          stage_dtype* dtype);

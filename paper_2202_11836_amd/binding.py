@@ -30,7 +30,7 @@ ALLOC_STATUS_NAMES = {0: "OK", 1: "EINVAL", 2: "ENOFIT"}
 EXPORTED = ("alloc_coarse", "alloc_fine", "alloc_workloads", "stage_init", "stage_set_stream", "stage_forward", "stage_backward", "stage_param",
             "stage_grad", "stage_set_param", "stage_read", "stage_tensor_bytes",
             "stage_trace_site", "stage_trace_mask", "stage_trace_read", "stage_site_count",
-            "stage_site_name",
+            "stage_site_name", "stage_device_bytes", "stage_memory_model",
             "stage_last_error", "stage_destroy")
 
 _lib = None
@@ -94,6 +94,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.stage_last_error.restype = ctypes.c_char_p
     lib.stage_destroy.argtypes = [vp]
     lib.stage_destroy.restype = None
+    lib.stage_device_bytes.argtypes = [vp, ctypes.POINTER(i64)]
+    lib.stage_device_bytes.restype = i32
+    lib.stage_memory_model.argtypes = [i32, i32, i32, i32, i32, i32, ctypes.POINTER(i64),
+                                       ctypes.POINTER(i64)]
+    lib.stage_memory_model.restype = i32
     dp, ip = ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)
     lib.alloc_coarse.argtypes = [i32, i32, dp, dp, ip, ip]
     lib.alloc_coarse.restype = i32
@@ -199,6 +204,20 @@ def stage_site_name(site: int) -> str:
     return load_library().stage_site_name(site).decode()
 
 
+def stage_device_bytes(handle) -> int:
+    v = ctypes.c_int64(0)
+    _check(handle, load_library().stage_device_bytes(handle, ctypes.byref(v)))
+    return v.value
+
+
+def stage_memory_model(hidden: int, heads: int, ffn: int, batch: int, seq: int, dtype: int):
+    """(per_layer, shared) device bytes of a stage after a forward of batch x seq."""
+    a, b = ctypes.c_int64(0), ctypes.c_int64(0)
+    _check(None, load_library().stage_memory_model(hidden, heads, ffn, batch, seq, dtype,
+                                                   ctypes.byref(a), ctypes.byref(b)))
+    return a.value, b.value
+
+
 def stage_last_error(handle) -> str:
     raw = load_library().stage_last_error(handle)
     return raw.decode() if raw else ""
@@ -298,6 +317,9 @@ class Stage:
             mask |= 1 << names.index(n)
         self._sync_stream()
         stage_trace_mask(self.handle, mask)
+
+    def device_bytes(self) -> int:
+        return stage_device_bytes(self.handle)
 
     def trace_read(self):
         """(launches, total_ms) of the traced site since trace() / the last read."""

@@ -757,6 +757,11 @@ hipError_t gemm_bf16(const GemmArgs& g, bool a_kmajor, bool b_kmajor, GemmEpi ep
   if (g.ksplit > 1 && g.kchunk % 64 != 0) return hipErrorInvalidValue;
   if ((a_kmajor || b_kmajor) && g.K % 64 != 0) return hipErrorInvalidValue;
   if ((!a_kmajor && g.M % 8 != 0) || (g.lda % 8 != 0) || (g.ldb % 8 != 0)) return hipErrorInvalidValue;
+  // Operands are read through buffer resources with 32-bit byte extents and
+  // offsets: each operand (per batch entry) must span less than 2 GiB.
+  const int64_t a_bytes = (int64_t)(a_kmajor ? g.M : g.K) * g.lda * 2;
+  const int64_t b_bytes = (int64_t)(b_kmajor ? g.N : g.K) * g.ldb * 2;
+  if (a_bytes >= ((int64_t)1 << 31) || b_bytes >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
   int tile = g.tile;
   if (tile == 0) {
     const int64_t t256 = (int64_t)((g.M + 255) / 256) * ((g.N + 255) / 256) * batch * g.ksplit;

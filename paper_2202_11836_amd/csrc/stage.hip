@@ -116,6 +116,10 @@ struct stage {
   std::vector<std::array<void*, STAGE_NPARAM>> param;
   std::vector<std::array<float*, STAGE_NPARAM>> grad;
   std::vector<void*> allocs;  // parameter / gradient memory
+  // Bytes requested from hipMalloc (parameters and gradients; activation
+  // record and workspace).  A dry-run stage only counts them.
+  int64_t bytes_param = 0, bytes_act = 0;
+  bool dry_run = false;
 
   // Activation memory, sized for cap_T tokens and cap_BSS score entries.
   int64_t cap_T = -1, cap_BSS = -1, cap_B = -1, cap_NQB = -1;
@@ -227,6 +231,7 @@ void free_activations(stage_t* s) {
   for (void* p : s->act_allocs) (void)hipFree(p);
   s->act_allocs.clear();
   s->saved.clear();
+  s->bytes_act = 0;
   s->cap_T = s->cap_BSS = s->cap_B = s->cap_NQB = -1;
   s->have_ctx = false;
 }
@@ -234,6 +239,8 @@ void free_activations(stage_t* s) {
 stage_status dev_alloc(stage_t* s, std::vector<void*>& list, void** p, size_t bytes) {
   *p = nullptr;
   if (bytes == 0) bytes = 256;
+  (&list == &s->allocs ? s->bytes_param : s->bytes_act) += (int64_t)bytes;
+  if (s->dry_run) return STAGE_OK;
   hipError_t e = hipMalloc(p, bytes);
   if (e != hipSuccess) {
     *p = nullptr;
@@ -740,7 +747,9 @@ stage_status stage_forward(stage_t* s, const void* x, const uint8_t* key_mask, i
   const int64_t T = (int64_t)batch * seq;
   if (T > 0 && (!x || !y)) return fail(s, STAGE_EINVAL, "null x or y");
   if (T > 0 && x == y) return fail(s, STAGE_EINVAL, "x and y may not alias");
-  if (T * std::max(3 * s->h, s->f) >= (int64_t)1 << 31)
+  // bf16 GEMM operands are read through buffer resources (32-bit byte
+  // extents): the widest activation, [T, max(3h, f)], must stay below 2 GiB.
+  if (T * std::max(3 * s->h, s->f) * (s->dtype == STAGE_BF16 ? 2 : 1) >= (int64_t)1 << 31)
     return fail(s, STAGE_EINVAL, "batch * seq too large");
   if (s->dtype == STAGE_F32 && (int64_t)batch * s->H * seq * seq >= (int64_t)1 << 40)
     return fail(s, STAGE_EINVAL, "score matrix too large");
@@ -899,6 +908,48 @@ stage_status stage_trace_read(stage_t* s, int* launches, double* total_ms) {
   s->events_used = 0;
   if (launches) *launches = n;
   if (total_ms) *total_ms = tot;
+  return STAGE_OK;
+}
+
+stage_status stage_device_bytes(const stage_t* s, int64_t* bytes) {
+  if (!s || !bytes) return STAGE_EINVAL;
+  *bytes = s->bytes_param + s->bytes_act;
+  return STAGE_OK;
+}
+
+stage_status stage_memory_model(int hidden, int heads, int ffn, int batch, int seq,
+                                stage_dtype dtype, int64_t* per_layer, int64_t* shared) {
+  if (!per_layer || !shared) return STAGE_EINVAL;
+  if (hidden < 64 || hidden % 64 || hidden > 2048 || heads < 1 || hidden % heads ||
+      hidden / heads != HEAD_DIM || ffn < 64 || ffn % 64 || batch < 0 || seq < 0 ||
+      (dtype != STAGE_F32 && dtype != STAGE_BF16))
+    return STAGE_EINVAL;
+  // The same allocation calls as stage_init and stage_forward, on stages
+  // that only count bytes: one layer and two layers.
+  int64_t act[2] = {0, 0}, par = 0;
+  for (int L = 1; L <= 2; ++L) {
+    stage_t d;
+    d.dry_run = true;
+    d.L = L;
+    d.h = hidden;
+    d.H = heads;
+    d.f = ffn;
+    d.dtype = dtype;
+    d.esz = dtype == STAGE_BF16 ? 2 : 4;
+    if (L == 1) {
+      for (int w = 0; w < STAGE_NPARAM; ++w) {
+        void* p;
+        const int64_t n = param_numel(&d, w);
+        (void)dev_alloc(&d, d.allocs, &p, n * param_esz(&d, w));
+        (void)dev_alloc(&d, d.allocs, &p, n * 4);
+      }
+      par = d.bytes_param;
+    }
+    if (ensure_activations(&d, batch, seq) != STAGE_OK) return STAGE_EINVAL;
+    act[L - 1] = d.bytes_act;
+  }
+  *per_layer = par + (act[1] - act[0]);
+  *shared = act[0] - (act[1] - act[0]);
   return STAGE_OK;
 }
 
