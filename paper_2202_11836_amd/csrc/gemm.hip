@@ -450,7 +450,10 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
           for (int i = 0; i < TM; ++i) af[nxt][i] = pa.get(i, ks + 1);
 #pragma unroll
           for (int j = 0; j < TN; ++j) bfr[nxt][j] = pb.get(j, ks + 1);
-        } else if (t + 1 < ntiles) {
+        } else {
+          // Unconditional (also for the last k-tile, whose "next" fragments
+          // are never used): a branch here would make the compiler wait for
+          // these reads before the last k-step's MFMAs.
           wait_ktile<C::DMA_PER_TILE, NS>(min(ntiles - 1, t + NS - 1) - (t + 1));
           __syncthreads();
           if (t + NS < ntiles) issue_ktile<BM, BN, AK, BKM>(g, T, t + NS, smem, wave, lane);
