@@ -50,10 +50,9 @@ __device__ __forceinline__ f32x16_t zero16() {
 
 // Registers r0 .. r0+7 of an accumulator as a bf16 operand.
 __device__ __forceinline__ bf16x8_t pack8(const f32x16_t& a, int r0) {
-  bf16x8_t v;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) v[i] = (__bf16)a[r0 + i];
-  return v;
+  const u32x4_t w = {pack_bf16x2(a[r0], a[r0 + 1]), pack_bf16x2(a[r0 + 2], a[r0 + 3]),
+                     pack_bf16x2(a[r0 + 4], a[r0 + 5]), pack_bf16x2(a[r0 + 6], a[r0 + 7])};
+  return __builtin_bit_cast(bf16x8_t, w);
 }
 
 __device__ __forceinline__ bf16x8_t ld_frag(const bf16_t* p) { return *(const bf16x8_t*)p; }
@@ -139,10 +138,8 @@ __device__ __forceinline__ void store_rows_t(const f32x16_t acc[2], float mul, b
     for (int q = 0; q < 4; ++q) {
       // registers 4q .. 4q+3 are 4 consecutive columns
       const int col = 32 * t + 8 * q + 4 * hf;
-      uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[t][4 * q] * mul)) |
-                    ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[t][4 * q + 1] * mul)) << 16);
-      uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[t][4 * q + 2] * mul)) |
-                    ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[t][4 * q + 3] * mul)) << 16);
+      const uint32_t lo = pack_bf16x2(acc[t][4 * q] * mul, acc[t][4 * q + 1] * mul);
+      const uint32_t hi = pack_bf16x2(acc[t][4 * q + 2] * mul, acc[t][4 * q + 3] * mul);
       *(u32x2_t*)(stage + rr * LD + col) = u32x2_t{lo, hi};
     }
   __builtin_amdgcn_s_waitcnt(0);

@@ -17,12 +17,16 @@ __device__ __forceinline__ float bf2f(bf16_t v) {
   return __uint_as_float(((uint32_t)v) << 16);
 }
 
-// Round-to-nearest-even fp32 -> bf16 (NaN kept quiet).
-__device__ __forceinline__ bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// fp32 -> bf16, round to nearest even (the hardware conversion).
+__device__ __forceinline__ bf16_t f2bf(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
+
+// Two fp32 values -> one packed pair of bf16 (lo in bits 0-15), round to
+// nearest even, in a single conversion instruction.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
 
 // Storage conversions: T is float or bf16_t.
@@ -47,32 +51,29 @@ __device__ __forceinline__ float wave_max(float v) {
 }
 
 // GELU u * Phi(u) = u/2 * (1 + erf(u / sqrt 2)) and its derivative
-// Phi(u) + u * phi(u).  erf is evaluated with the rational approximation of
-// Abramowitz & Stegun, Handbook of Mathematical Functions, formula 7.1.26
-// (after Hastings): erf(x) = 1 - (a1 t + ... + a5 t^5) exp(-x^2),
-// t = 1 / (1 + p x), x >= 0, |error| <= 1.5e-7.  It is branch-free, and the
-// exp(-x^2) = exp(-u^2 / 2) term is shared with the derivative.
-struct ErfParts {
-  float onep;  // 1 + erf(u / sqrt 2) = 2 Phi(u), without cancellation for u < 0
-  float e;     // exp(-u^2 / 2)
+// Phi(u) + u * phi(u).  erfc(|u| / sqrt 2) is evaluated with the rational
+// approximation of Abramowitz & Stegun, Handbook of Mathematical Functions,
+// formula 7.1.26 (after Hastings): erfc(x) = (a1 t + ... + a5 t^5) exp(-x^2),
+// t = 1 / (1 + p x), x >= 0, |error| <= 1.5e-7, with its coefficients halved
+// so that the polynomial yields erfc / 2 = min(Phi(u), 1 - Phi(u)) directly.
+// It is branch-free, and exp(-x^2) = exp(-u^2 / 2) is shared with the
+// derivative.
+struct GeluParts {
+  float cdf;  // Phi(u), without cancellation for u < 0
+  float e;    // exp(-u^2 / 2)
 };
-__device__ __forceinline__ ErfParts erf_parts(float u) {
-  const float x = u * 0.70710678118654752f;
-  const float ax = fabsf(x);
-  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, ax, 1.0f));
-  const float poly =
-      t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, 1.061405429f, -1.453152027f), 1.421413741f),
-                       -0.284496736f),
-               0.254829592f);
-  const float e = __builtin_amdgcn_exp2f(-x * x * 1.4426950408889634f);
-  const float erfc_ax = poly * e;  // 1 - erf(|x|)
-  return {x < 0.0f ? erfc_ax : 2.0f - erfc_ax, e};
+__device__ __forceinline__ GeluParts gelu_parts(float u) {
+  const float t = __builtin_amdgcn_rcpf(fmaf(fabsf(u), 0.3275911f * 0.70710678118654752f, 1.0f));
+  const float hp =
+      t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, 0.5307027145f, -0.7265760135f), 0.7107068705f),
+                       -0.142248368f),
+               0.127414796f);
+  const float e = __builtin_amdgcn_exp2f(u * (u * -0.72134752044448170f));  // exp(-u^2/2)
+  const float h = hp * e;  // erfc(|u| / sqrt 2) / 2
+  return {u < 0.0f ? h : 1.0f - h, e};
 }
-__device__ __forceinline__ float gelu_f(float u) {
-  const ErfParts p = erf_parts(u);
-  return 0.5f * u * p.onep;
-}
+__device__ __forceinline__ float gelu_f(float u) { return u * gelu_parts(u).cdf; }
 __device__ __forceinline__ float gelu_grad_f(float u) {
-  const ErfParts p = erf_parts(u);
-  return fmaf(u * 0.39894228040143268f, p.e, 0.5f * p.onep);
+  const GeluParts p = gelu_parts(u);
+  return fmaf(u * 0.39894228040143268f, p.e, p.cdf);
 }

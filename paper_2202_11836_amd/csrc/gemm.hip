@@ -225,10 +225,6 @@ struct FragPtrs {
   }
 };
 
-__device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
-  return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)a) |
-         ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)b) << 16);
-}
 
 // Epilogue for 8 consecutive columns n..n+7 of row m (n % 8 == 0, n < N).
 // For EPI_MUL, v returns the values as stored.
@@ -284,12 +280,12 @@ __device__ __forceinline__ void epi8(const GemmArgs& g, int64_t offC, int zs, in
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
         const float u = v[2 * i + e];
-        const ErfParts p = erf_parts(u);
-        gv[e] = 0.5f * u * p.onep;
-        dv[e] = fmaf(u * 0.39894228040143268f, p.e, 0.5f * p.onep);
+        const GeluParts p = gelu_parts(u);
+        gv[e] = u * p.cdf;
+        dv[e] = fmaf(u * 0.39894228040143268f, p.e, p.cdf);
       }
-      o[i] = pack_bf2(gv[0], gv[1]);
-      q[i] = pack_bf2(dv[0], dv[1]);
+      o[i] = pack_bf16x2(gv[0], gv[1]);
+      q[i] = pack_bf16x2(dv[0], dv[1]);
     }
     *(u32x4_t*)((bf16_t*)g.C + offC + idx) = o;
     *(u32x4_t*)((bf16_t*)g.C2 + offC + idx) = q;
@@ -297,7 +293,7 @@ __device__ __forceinline__ void epi8(const GemmArgs& g, int64_t offC, int zs, in
   }
   u32x4_t o;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) o[i] = pack_bf2(v[2 * i], v[2 * i + 1]);
+  for (int i = 0; i < 4; ++i) o[i] = pack_bf16x2(v[2 * i], v[2 * i + 1]);
   *(u32x4_t*)((bf16_t*)g.C + offC + idx) = o;
   if (EPI == EPI_MUL) {  // hand back the stored (rounded) values
 #pragma unroll

@@ -29,7 +29,7 @@ __device__ __forceinline__ void load8(const float* p, float v[8]) {
 __device__ __forceinline__ void store8(bf16_t* p, const float v[8]) {
   u32x4_t r;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) r[i] = (uint32_t)f2bf(v[2 * i]) | ((uint32_t)f2bf(v[2 * i + 1]) << 16);
+  for (int i = 0; i < 4; ++i) r[i] = pack_bf16x2(v[2 * i], v[2 * i + 1]);
   *(u32x4_t*)p = r;
 }
 __device__ __forceinline__ void store8(float* p, const float v[8]) {
