@@ -41,6 +41,13 @@ __device__ __forceinline__ f32x16_t mfma32(bf16x8_t a, bf16x8_t b, f32x16_t c) {
 // Row of register r in a 32x32 accumulator for lane half hf.
 __device__ __forceinline__ int acc_row(int r, int hf) { return 8 * (r >> 2) + 4 * hf + (r & 3); }
 
+__device__ __forceinline__ f32x16_t splat16(float v) {
+  f32x16_t z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = v;
+  return z;
+}
+
 __device__ __forceinline__ f32x16_t zero16() {
   f32x16_t z;
 #pragma unroll
@@ -190,12 +197,24 @@ __global__ __launch_bounds__(256) void key_extent_kernel(const uint8_t* __restri
   if (threadIdx.x == 0) kext[b] = max(max(sm[0], sm[1]), max(sm[2], sm[3]));
 }
 
+// Called by all 64 lanes of wavefront 0 with the bias (0 or -inf) of key
+// `lane` of a 64-key block: flags[i] = 1 if none of keys 32 i .. 32 i + 31
+// is masked.
+__device__ __forceinline__ void store_kfull(int* flags, float bias, int lane) {
+  const uint64_t ok = __ballot(bias == 0.0f);
+  if (lane == 0) {
+    flags[0] = (uint32_t)ok == 0xffffffffu;
+    flags[1] = (uint32_t)(ok >> 32) == 0xffffffffu;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Forward: wavefront = 32 queries; block = 128 queries of one (batch, head).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) char tiles[2][2 * TILE];  // per stage: K, V
   __shared__ __attribute__((aligned(16))) float kbias[2][KT];         // 0 or -inf per key
+  __shared__ int kfull[2][2];  // per stage and 32-key half: no key masked
 
   const int bh = blockIdx.y, b = bh / a.H, j = bh % a.H;
   const int S = a.S, h = a.h;
@@ -215,7 +234,11 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
   };
 
   if (nkb > 0) {
-    if (tid < KT) kbias[0][tid] = bias_of(0);
+    if (tid < KT) {  // wavefront 0
+      const float kb0 = bias_of(0);
+      kbias[0][tid] = kb0;
+      store_kfull(kfull[0], kb0, tid);
+    }
     dma_rows(rsK, 0, ld, tiles[0], wave, lane);
     dma_rows(rsV, 0, ld, tiles[0] + TILE, wave, lane);
   }
@@ -252,14 +275,25 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
       f32x16_t s = zero16();
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) s = mfma32(frag_rows(Ks, 32 * sub, ks, lane), qf[ks], s);
+      // No masked key in these 32: the scale is applied inside the exponent
+      // below (the block maximum scales with it); else the scaled scores
+      // get the key bias (0 or -inf) here.
+      const bool full = __builtin_amdgcn_readfirstlane(kfull[st][sub]) != 0;
+      const float c = full ? a.scale_log2 : 1.0f;
       float mblk = -INFINITY;
+      if (full) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4_t kbv = *(const f32x4_t*)&kbias[st][32 * sub + 8 * g + 4 * hf];
+        for (int r = 0; r < 16; ++r) mblk = fmaxf(mblk, s[r]);
+        mblk *= a.scale_log2;
+      } else {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          s[4 * g + e] = fmaf(s[4 * g + e], a.scale_log2, kbv[e]);
-          mblk = fmaxf(mblk, s[4 * g + e]);
+        for (int g = 0; g < 4; ++g) {
+          const f32x4_t kbv = *(const f32x4_t*)&kbias[st][32 * sub + 8 * g + 4 * hf];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            s[4 * g + e] = fmaf(s[4 * g + e], a.scale_log2, kbv[e]);
+            mblk = fmaxf(mblk, s[4 * g + e]);
+          }
         }
       }
       mblk = fmaxf(mblk, __shfl_xor(mblk, 32, 64));
@@ -281,7 +315,7 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
       float ps = 0.0f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        s[r] = __builtin_amdgcn_exp2f(s[r] - off);
+        s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], c, -off));
         ps += s[r];
       }
       lsum += ps;
@@ -294,7 +328,10 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
           acc[t] = mfma32(frag_tr(Vs, 32 * t, 32 * sub + 16 * ks, lane), pb, acc[t]);
       }
     }
-    if (kb + 1 < nkb && tid < KT) kbias[st ^ 1][tid] = nbias;
+    if (kb + 1 < nkb && tid < KT) {
+      kbias[st ^ 1][tid] = nbias;
+      store_kfull(kfull[st ^ 1], nbias, tid);
+    }
   }
   const float ltot = lsum + __shfl_xor(lsum, 32, 64);
   const float inv = ltot > 0.0f ? 1.0f / ltot : 0.0f;
@@ -311,6 +348,7 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
 __global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) char tiles[2][2 * TILE];  // per stage: K, V
   __shared__ __attribute__((aligned(16))) float kbias[2][KT];
+  __shared__ int kfull[2][2];  // per stage and 32-key half: no key masked
 
   const int bh = blockIdx.y, b = bh / a.H, j = bh % a.H;
   const int S = a.S, h = a.h;
@@ -333,7 +371,11 @@ __global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
   };
 
   if (nkb > 0) {
-    if (tid < KT) kbias[0][tid] = bias_of(0);
+    if (tid < KT) {  // wavefront 0
+      const float kb0 = bias_of(0);
+      kbias[0][tid] = kb0;
+      store_kfull(kfull[0], kb0, tid);
+    }
     dma_rows(rsK, 0, ld, tiles[0], wave, lane);
     dma_rows(rsV, 0, ld, tiles[0] + TILE, wave, lane);
   }
@@ -373,21 +415,27 @@ __global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
 #pragma unroll
     for (int sub = 0; sub < KT / 32; ++sub) {
       if (kb * KT + 32 * sub >= kend) break;
-      // S^T = K_sub Q^T and dP^T = V_sub dO^T (keys x queries)
-      f32x16_t s = zero16(), dp = zero16();
+      // S^T = K_sub Q^T and dP^T - D = V_sub dO^T - D (keys x queries; the
+      // accumulator starts at -D of the lane's query)
+      f32x16_t s = zero16(), dp = splat16(-dsum);
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         s = mfma32(frag_rows(Ks, 32 * sub, ks, lane), qf[ks], s);
         dp = mfma32(frag_rows(Vs, 32 * sub, ks, lane), dof[ks], dp);
       }
+      if (__builtin_amdgcn_readfirstlane(kfull[st][sub])) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4_t kbv = *(const f32x4_t*)&kbias[st][32 * sub + 8 * g + 4 * hf];
+        for (int r = 0; r < 16; ++r)  // dS^T (unscaled)
+          s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, -lse_q)) * dp[r];
+      } else {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = 4 * g + e;
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, kbv[e]) - lse_q);
-          s[r] = p * (dp[r] - dsum);  // dS^T (unscaled)
+        for (int g = 0; g < 4; ++g) {
+          const f32x4_t kbv = *(const f32x4_t*)&kbias[st][32 * sub + 8 * g + 4 * hf];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int r = 4 * g + e;
+            s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, kbv[e]) - lse_q) * dp[r];
+          }
         }
       }
       // dQ^T += K^T dS^T
@@ -399,7 +447,10 @@ __global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
           dq[t] = mfma32(frag_tr(Ks, 32 * t, 32 * sub + 16 * ks, lane), db, dq[t]);
       }
     }
-    if (kb + 1 < nkb && tid < KT) kbias[st ^ 1][tid] = nbias;
+    if (kb + 1 < nkb && tid < KT) {
+      kbias[st ^ 1][tid] = nbias;
+      store_kfull(kfull[st ^ 1], nbias, tid);
+    }
   }
   __syncthreads();  // the ring becomes the output staging area
   bf16_t* stage = (bf16_t*)&tiles[0][0] + wave * 32 * LD;
@@ -427,6 +478,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
   const int kend = a.kext[b];
   const int key = k0 + rr;
   const bool kvalid = key < kend && a.mask[(int64_t)b * S + key] != 0;
+  const bool kall = __all(kvalid);  // none of this wavefront's 32 keys is masked
   const bool block_live = blockIdx.x * 128 < kend;  // uniform over the block
   const int nqb = block_live ? (S + KT - 1) / KT : 0;
   const __amdgpu_buffer_rsrc_t rsQ = rows_rsrc(Qg, S, ld), rsD = rows_rsrc(dOg, S, h);
@@ -470,8 +522,15 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
 #pragma unroll
     for (int sub = 0; sub < KT / 32; ++sub) {
       if (qb * KT + 32 * sub >= S) break;
-      // S (32 queries x 32 keys) = Q_sub K^T;  dP = dO_sub V^T
-      f32x16_t s = zero16(), dp = zero16();
+      // S (32 queries x 32 keys) = Q_sub K^T;  dP - D = dO_sub V^T - D (the
+      // accumulator starts at -D of each register's query)
+      f32x16_t s = zero16(), dp;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4_t dv4 = *(const f32x4_t*)&rowv[st][1][32 * sub + 8 * g + 4 * hf];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) dp[4 * g + e] = -dv4[e];
+      }
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         s = mfma32(frag_rows(Qs, 32 * sub, ks, lane), kf[ks], s);
@@ -480,13 +539,13 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const f32x4_t lv = *(const f32x4_t*)&rowv[st][0][32 * sub + 8 * g + 4 * hf];
-        const f32x4_t dv4 = *(const f32x4_t*)&rowv[st][1][32 * sub + 8 * g + 4 * hf];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = 4 * g + e;
-          const float p = kvalid ? __builtin_amdgcn_exp2f(s[r] * a.scale_log2 - lv[e]) : 0.0f;
+          float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, -lv[e]));
+          if (!kall) p = kvalid ? p : 0.0f;
           s[r] = p;
-          dp[r] = p * (dp[r] - dv4[e]);  // dS (unscaled)
+          dp[r] = p * dp[r];  // dS (unscaled)
         }
       }
       // dV^T += dO^T P;  dK^T += Q^T dS
