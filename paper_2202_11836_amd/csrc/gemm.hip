@@ -665,13 +665,27 @@ __global__ __launch_bounds__(NT) void gemm_f32_kernel(GemmArgs g) {
     }
 }
 
-__global__ void splitk_reduce_kernel(const float* __restrict__ part, int splits, int64_t mn,
-                                     float* __restrict__ out) {
-  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// out = sum over splits of part[z] in split order; 4 consecutive values per
+// thread (mn % 4 == 0), all splits' loads issued before the sum.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part,
+                                                            int splits, int64_t mn,
+                                                            float* __restrict__ out) {
+  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (i >= mn) return;
-  float s = 0.0f;
-  for (int z = 0; z < splits; ++z) s += part[(int64_t)z * mn + i];
-  out[i] = s;
+  f32x4_t s = *(const f32x4_t*)(part + i);
+  int z = 1;
+  for (; z + 4 <= splits; z += 4) {
+    const f32x4_t a = *(const f32x4_t*)(part + (int64_t)z * mn + i);
+    const f32x4_t b = *(const f32x4_t*)(part + (int64_t)(z + 1) * mn + i);
+    const f32x4_t c = *(const f32x4_t*)(part + (int64_t)(z + 2) * mn + i);
+    const f32x4_t d = *(const f32x4_t*)(part + (int64_t)(z + 3) * mn + i);
+    s += a;
+    s += b;
+    s += c;
+    s += d;
+  }
+  for (; z < splits; ++z) s += *(const f32x4_t*)(part + (int64_t)z * mn + i);
+  *(f32x4_t*)(out + i) = s;
 }
 
 int device_cus() {
@@ -784,7 +798,8 @@ hipError_t splitk_reduce(const float* part, int splits, int M, int N, float* out
                          hipStream_t st) {
   int64_t mn = (int64_t)M * N;
   if (mn == 0) return hipSuccess;
-  int blocks = (int)((mn + 255) / 256);
+  if (mn % 4 != 0 || splits < 1) return hipErrorInvalidValue;
+  int blocks = (int)((mn / 4 + 255) / 256);
   hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, st, part, splits, mn, out);
   return hipGetLastError();
 }

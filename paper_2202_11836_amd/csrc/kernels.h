@@ -78,7 +78,7 @@ hipError_t add_ln_fwd(const TA* a, const float* bias, const TR* resid, const flo
 // Column partial sums per block of LN_BWD_RPB rows (ln_bwd_blocks(rows)
 // blocks): part[blk][0][:] = sum dy*xhat, part[blk][1][:] = sum dy,
 // part[blk][2][:] = sum dz.
-constexpr int LN_BWD_RPB = 16;
+constexpr int LN_BWD_RPB = 32;
 int ln_bwd_blocks(int rows);
 template <typename T>
 hipError_t ln_bwd(const T* dy, const T* xhat, const float* rstd, const float* gamma, T* dz,
