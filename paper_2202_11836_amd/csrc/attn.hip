@@ -85,13 +85,14 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const bf16_t* base, 
                                            0x00020000);
 }
 
-// Rows [row0, row0 + 64) into a tile with direct-to-LDS loads: 8 loads of
-// 8 rows (lane l's 16 bytes land at +16 l), two per wavefront.
+// Rows [row0, row0 + NR) into a tile with direct-to-LDS loads: NR / 8 loads
+// of 8 rows (lane l's 16 bytes land at +16 l), NR / 32 per wavefront.
+template <int NR = KT>
 __device__ __forceinline__ void dma_rows(__amdgpu_buffer_rsrc_t rs, int row0, int64_t ld,
                                          char* tile, int wave, int lane) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int q = 2 * wave + i;
+  for (int i = 0; i < NR / 32; ++i) {
+    const int q = (NR / 32) * wave + i;
     const int r = 8 * q + (lane >> 3);
     const int c = (lane & 7) ^ tswz(r);
     const int64_t off = ((int64_t)(row0 + r) * ld + 8 * c) * 2;
@@ -460,11 +461,15 @@ __global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Backward, dK and dV: wavefront = 32 keys; loops over query blocks.
+// Backward, dK and dV: wavefront = 32 keys; loops over query blocks of QB
+// (twice the key block: two barriers per 256 queries instead of four, with
+// two resident blocks per CU as the registers allow).
 // ---------------------------------------------------------------------------
+constexpr int QB = 2 * KT;
+constexpr int QTILE = QB * HD * 2;
 __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(1024))) char tiles[2][2 * TILE];  // per stage: Q, dO
-  __shared__ __attribute__((aligned(16))) float rowv[2][2][KT];       // per stage: lse, D
+  __shared__ __attribute__((aligned(1024))) char tiles[2][2 * QTILE];  // per stage: Q, dO
+  __shared__ __attribute__((aligned(16))) float rowv[2][2][QB];        // per stage: lse, D
 
   const int bh = blockIdx.y, b = bh / a.H, j = bh % a.H;
   const int S = a.S, h = a.h;
@@ -480,19 +485,20 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
   const bool kvalid = key < kend && a.mask[(int64_t)b * S + key] != 0;
   const bool kall = __all(kvalid);  // none of this wavefront's 32 keys is masked
   const bool block_live = blockIdx.x * 128 < kend;  // uniform over the block
-  const int nqb = block_live ? (S + KT - 1) / KT : 0;
+  const int nqb = block_live ? (S + QB - 1) / QB : 0;
   const __amdgpu_buffer_rsrc_t rsQ = rows_rsrc(Qg, S, ld), rsD = rows_rsrc(dOg, S, h);
-  // threads 0-63 carry lse, 64-127 D of query block qb (rows past S: P = 0)
+  // threads 0-127 carry lse, 128-255 D of query block qb (rows past S: P = 0)
+  static_assert(2 * QB == 256, "one value per thread");
   auto rowval = [&](int qb) {
-    const int qq = qb * KT + (tid & 63);
-    if (tid < KT) return qq < S ? a.lse[(int64_t)bh * S + qq] : INFINITY;
+    const int qq = qb * QB + (tid & (QB - 1));
+    if (tid < QB) return qq < S ? a.lse[(int64_t)bh * S + qq] : INFINITY;
     return qq < S ? a.dsum[(int64_t)bh * S + qq] : 0.0f;
   };
 
   if (nqb > 0) {
-    if (tid < 2 * KT) rowv[0][tid >> 6][tid & 63] = rowval(0);
-    dma_rows(rsQ, 0, ld, tiles[0], wave, lane);
-    dma_rows(rsD, 0, h, tiles[0] + TILE, wave, lane);
+    rowv[0][tid / QB][tid & (QB - 1)] = rowval(0);
+    dma_rows<QB>(rsQ, 0, ld, tiles[0], wave, lane);
+    dma_rows<QB>(rsD, 0, h, tiles[0] + QTILE, wave, lane);
   }
   bf16x8_t kf[4], vf[4];
 #pragma unroll
@@ -513,15 +519,15 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
     __syncthreads();
     float nrow = 0.0f;
     if (qb + 1 < nqb) {
-      if (tid < 2 * KT) nrow = rowval(qb + 1);
-      dma_rows(rsQ, (qb + 1) * KT, ld, tiles[st ^ 1], wave, lane);
-      dma_rows(rsD, (qb + 1) * KT, h, tiles[st ^ 1] + TILE, wave, lane);
+      nrow = rowval(qb + 1);
+      dma_rows<QB>(rsQ, (qb + 1) * QB, ld, tiles[st ^ 1], wave, lane);
+      dma_rows<QB>(rsD, (qb + 1) * QB, h, tiles[st ^ 1] + QTILE, wave, lane);
     }
     const char* Qs = tiles[st];
-    const char* dOs = tiles[st] + TILE;
+    const char* dOs = tiles[st] + QTILE;
 #pragma unroll
-    for (int sub = 0; sub < KT / 32; ++sub) {
-      if (qb * KT + 32 * sub >= S) break;
+    for (int sub = 0; sub < QB / 32; ++sub) {
+      if (qb * QB + 32 * sub >= S) break;
       // S (32 queries x 32 keys) = Q_sub K^T;  dP - D = dO_sub V^T - D (the
       // accumulator starts at -D of each register's query)
       f32x16_t s = zero16(), dp;
@@ -560,7 +566,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
         }
       }
     }
-    if (qb + 1 < nqb && tid < 2 * KT) rowv[st ^ 1][tid >> 6][tid & 63] = nrow;
+    if (qb + 1 < nqb) rowv[st ^ 1][tid / QB][tid & (QB - 1)] = nrow;
   }
   __syncthreads();  // the ring becomes the output staging area
   bf16_t* stage = (bf16_t*)&tiles[0][0] + wave * 32 * LD;
