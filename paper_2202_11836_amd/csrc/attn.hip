@@ -198,6 +198,20 @@ __global__ __launch_bounds__(256) void key_extent_kernel(const uint8_t* __restri
   if (threadIdx.x == 0) kext[b] = max(max(sm[0], sm[1]), max(sm[2], sm[3]));
 }
 
+// Work-group -> (row block, batch * head).  The grid is one-dimensional,
+// nq row blocks per (batch, head); consecutive work-groups go round robin
+// over the 8 XCDs, so they are remapped such that each XCD takes a
+// contiguous range and the row blocks of one (batch, head), which stream the
+// same keys and values (or queries and output gradients), share that XCD's
+// L2.
+__device__ __forceinline__ void attn_block(int nq, int& rb, int& bh) {
+  const int n = gridDim.x;
+  int w = blockIdx.x;
+  if ((n & 7) == 0) w = (w & 7) * (n >> 3) + (w >> 3);
+  rb = w % nq;
+  bh = w / nq;
+}
+
 // Called by all 64 lanes of wavefront 0 with the bias (0 or -inf) of key
 // `lane` of a 64-key block: flags[i] = 1 if none of keys 32 i .. 32 i + 31
 // is masked.
@@ -217,11 +231,13 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) float kbias[2][KT];         // 0 or -inf per key
   __shared__ int kfull[2][2];  // per stage and 32-key half: no key masked
 
-  const int bh = blockIdx.y, b = bh / a.H, j = bh % a.H;
+  int qb, bh;
+  attn_block((a.S + 127) / 128, qb, bh);
+  const int b = bh / a.H, j = bh % a.H;
   const int S = a.S, h = a.h;
   const int64_t ld = 3 * (int64_t)h;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hf = lane >> 5, rr = lane & 31;
-  const int q0 = blockIdx.x * 128 + wave * 32;
+  const int q0 = qb * 128 + wave * 32;
   const bf16_t* __restrict__ Qg = a.qkv + (int64_t)b * S * ld + j * HD;
   const bf16_t* __restrict__ Kg = Qg + h;
   const bf16_t* __restrict__ Vg = Qg + 2 * h;
@@ -351,11 +367,13 @@ __global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) float kbias[2][KT];
   __shared__ int kfull[2][2];  // per stage and 32-key half: no key masked
 
-  const int bh = blockIdx.y, b = bh / a.H, j = bh % a.H;
+  int qb, bh;
+  attn_block((a.S + 127) / 128, qb, bh);
+  const int b = bh / a.H, j = bh % a.H;
   const int S = a.S, h = a.h;
   const int64_t ld = 3 * (int64_t)h;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hf = lane >> 5, rr = lane & 31;
-  const int q0 = blockIdx.x * 128 + wave * 32;
+  const int q0 = qb * 128 + wave * 32;
   const bf16_t* __restrict__ Qg = a.qkv + (int64_t)b * S * ld + j * HD;
   const bf16_t* __restrict__ Kg = Qg + h;
   const bf16_t* __restrict__ Vg = Qg + 2 * h;
@@ -471,11 +489,13 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) char tiles[2][2 * QTILE];  // per stage: Q, dO
   __shared__ __attribute__((aligned(16))) float rowv[2][2][QB];        // per stage: lse, D
 
-  const int bh = blockIdx.y, b = bh / a.H, j = bh % a.H;
+  int kb128, bh;
+  attn_block((a.S + 127) / 128, kb128, bh);
+  const int b = bh / a.H, j = bh % a.H;
   const int S = a.S, h = a.h;
   const int64_t ld = 3 * (int64_t)h;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hf = lane >> 5, rr = lane & 31;
-  const int k0 = blockIdx.x * 128 + wave * 32;
+  const int k0 = kb128 * 128 + wave * 32;
   const bf16_t* __restrict__ Qg = a.qkv + (int64_t)b * S * ld + j * HD;
   const bf16_t* __restrict__ Kg = Qg + h;
   const bf16_t* __restrict__ Vg = Qg + 2 * h;
@@ -484,7 +504,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
   const int key = k0 + rr;
   const bool kvalid = key < kend && a.mask[(int64_t)b * S + key] != 0;
   const bool kall = __all(kvalid);  // none of this wavefront's 32 keys is masked
-  const bool block_live = blockIdx.x * 128 < kend;  // uniform over the block
+  const bool block_live = kb128 * 128 < kend;  // uniform over the block
   const int nqb = block_live ? (S + QB - 1) / QB : 0;
   const __amdgpu_buffer_rsrc_t rsQ = rows_rsrc(Qg, S, ld), rsD = rows_rsrc(dOg, S, h);
   // threads 0-127 carry lse, 128-255 D of query block qb (rows past S: P = 0)
@@ -588,21 +608,21 @@ hipError_t key_extent(const uint8_t* mask, int B, int S, int* kext, hipStream_t 
 
 hipError_t attn_forward(const AttnArgs& a, hipStream_t st) {
   if (a.B == 0 || a.S == 0) return hipSuccess;
-  dim3 grid((a.S + 127) / 128, a.B * a.H);
+  dim3 grid((unsigned)(((a.S + 127) / 128) * a.B * a.H));
   hipLaunchKernelGGL(attn_fwd_kernel, grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
 hipError_t attn_backward_dq(const AttnArgs& a, hipStream_t st) {
   if (a.B == 0 || a.S == 0) return hipSuccess;
-  dim3 grid((a.S + 127) / 128, a.B * a.H);
+  dim3 grid((unsigned)(((a.S + 127) / 128) * a.B * a.H));
   hipLaunchKernelGGL(attn_bwd_dq_kernel, grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
 hipError_t attn_backward_dkdv(const AttnArgs& a, hipStream_t st) {
   if (a.B == 0 || a.S == 0) return hipSuccess;
-  dim3 grid((a.S + 127) / 128, a.B * a.H);
+  dim3 grid((unsigned)(((a.S + 127) / 128) * a.B * a.H));
   hipLaunchKernelGGL(attn_bwd_dkdv_kernel, grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
