@@ -3,6 +3,8 @@
 // gamma / beta gradients, and the masked row softmax (forward and backward).
 // One wavefront owns one row; reductions across the row are wavefront
 // shuffles.  No MFMA here.
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace {
@@ -223,6 +225,132 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const T* __restrict__ dy,
     P[e] = ((red[e] + red[3 * h + e]) + red[6 * h + e]) + red[9 * h + e];
 }
 
+// bf16 LayerNorm backward with the rows kept as packed bf16 (unpacked where
+// used) and gamma in LDS, so that four wavefronts per SIMD fit: the same
+// arithmetic and partial rows as ln_bwd_kernel, twice the loads in flight.
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ float bf_at(const u32x4_t& r, int k) {
+  return (k & 1) ? bf_hi(r[k >> 1]) : bf_lo(r[k >> 1]);
+}
+
+template <int NC>
+__global__ __launch_bounds__(256, (NC <= 2 ? 3 : 1)) void ln_bwd_bf16_kernel(const bf16_t* __restrict__ dy,
+                                                            const bf16_t* __restrict__ xhat,
+                                                            const float* __restrict__ rstd,
+                                                            const float* __restrict__ gamma,
+                                                            bf16_t* __restrict__ dz,
+                                                            float* __restrict__ part, int rows,
+                                                            int h, int rpb) {
+  extern __shared__ float red[];  // [4 wavefronts][3][h], then gamma [h]
+  float* gsh = red + 12 * h;
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int nchunk = h >> 3;
+  for (int c = threadIdx.x; c < h; c += 256) gsh[c] = gamma[c];
+  __syncthreads();
+  float pg[NC][8], pb[NC][8], pz[NC][8];
+#pragma unroll
+  for (int i = 0; i < NC; ++i)
+#pragma unroll
+    for (int k = 0; k < 8; ++k) pg[i][k] = pb[i][k] = pz[i][k] = 0.0f;
+  const int r0 = blockIdx.x * rpb;
+  const int r1 = min(rows, r0 + rpb);
+  const float inv_h = 1.0f / (float)h;
+  for (int row0 = r0 + wave; row0 < r1; row0 += 8) {
+    u32x4_t dr[2][NC], xr[2][NC];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int row = row0 + 4 * u;
+      const int64_t base = (int64_t)row * h;
+#pragma unroll
+      for (int i = 0; i < NC; ++i) {
+        const int c = lane + 64 * i;
+        if (c < nchunk && row < r1) {
+          dr[u][i] = *(const u32x4_t*)(dy + base + 8 * c);
+          xr[u][i] = *(const u32x4_t*)(xhat + base + 8 * c);
+        } else {
+          dr[u][i] = xr[u][i] = u32x4_t{0, 0, 0, 0};
+        }
+      }
+    }
+    float sg[2] = {0.0f, 0.0f}, sgx[2] = {0.0f, 0.0f};
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      const int c = lane + 64 * i;
+      const int cc = c < nchunk ? c : 0;
+      const f32x4_t g0 = *(const f32x4_t*)(gsh + 8 * cc), g1 = *(const f32x4_t*)(gsh + 8 * cc + 4);
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const float d = bf_at(dr[u][i], k), x = bf_at(xr[u][i], k);
+          const float g = d * (k < 4 ? g0[k] : g1[k - 4]);
+          sg[u] += g;
+          sgx[u] += g * x;
+          pg[i][k] += d * x;
+          pb[i][k] += d;
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      sg[u] = wave_sum(sg[u]) * inv_h;
+      sgx[u] = wave_sum(sgx[u]) * inv_h;
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int row = row0 + 4 * u;
+      if (row >= r1) continue;
+      const int64_t base = (int64_t)row * h;
+      const float rs = rstd[row];
+#pragma unroll
+      for (int i = 0; i < NC; ++i) {
+        const int c = lane + 64 * i;
+        if (c < nchunk) {
+          const f32x4_t g0 = *(const f32x4_t*)(gsh + 8 * c), g1 = *(const f32x4_t*)(gsh + 8 * c + 4);
+          u32x4_t o;
+#pragma unroll
+          for (int k2 = 0; k2 < 4; ++k2) {
+            float dd[2];
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+              const int k = 2 * k2 + e;
+              const float d = bf_at(dr[u][i], k), x = bf_at(xr[u][i], k);
+              const float gm = k < 4 ? g0[k] : g1[k - 4];
+              dd[e] = rs * (d * gm - sg[u] - x * sgx[u]);
+            }
+            o[k2] = pack_bf16x2(dd[0], dd[1]);
+            // The column sum uses the value as stored, so that the bias
+            // gradient of the preceding linear layer matches the gradient
+            // that flows on.
+            pz[i][2 * k2] += bf_lo(o[k2]);
+            pz[i][2 * k2 + 1] += bf_hi(o[k2]);
+          }
+          *(u32x4_t*)(dz + base + 8 * c) = o;
+        }
+      }
+    }
+  }
+  float* mine = red + wave * 3 * h;
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const int c = lane + 64 * i;
+    if (c < nchunk) {
+      const int col = 8 * c;
+      *(f32x4_t*)(mine + col) = f32x4_t{pg[i][0], pg[i][1], pg[i][2], pg[i][3]};
+      *(f32x4_t*)(mine + col + 4) = f32x4_t{pg[i][4], pg[i][5], pg[i][6], pg[i][7]};
+      *(f32x4_t*)(mine + h + col) = f32x4_t{pb[i][0], pb[i][1], pb[i][2], pb[i][3]};
+      *(f32x4_t*)(mine + h + col + 4) = f32x4_t{pb[i][4], pb[i][5], pb[i][6], pb[i][7]};
+      *(f32x4_t*)(mine + 2 * h + col) = f32x4_t{pz[i][0], pz[i][1], pz[i][2], pz[i][3]};
+      *(f32x4_t*)(mine + 2 * h + col + 4) = f32x4_t{pz[i][4], pz[i][5], pz[i][6], pz[i][7]};
+    }
+  }
+  __syncthreads();
+  float* P = part + (int64_t)blockIdx.x * 3 * h;
+  for (int e = threadIdx.x; e < 3 * h; e += 256)
+    P[e] = ((red[e] + red[3 * h + e]) + red[6 * h + e]) + red[9 * h + e];
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void col_partial_kernel(const T* __restrict__ x, int rows, int n,
                                                           int rows_per_blk,
@@ -403,6 +531,16 @@ hipError_t ln_bwd(const T* dy, const T* xhat, const float* rstd, const float* ga
   dim3 grid(ln_bwd_blocks(rows)), blk(256);
   size_t sh = (size_t)4 * 3 * h * sizeof(float);
   const int rpb = LN_BWD_RPB;
+  if constexpr (std::is_same<T, bf16_t>::value) {
+    sh += (size_t)h * sizeof(float);
+    switch (nc) {
+      case 1: hipLaunchKernelGGL((ln_bwd_bf16_kernel<1>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
+      case 2: hipLaunchKernelGGL((ln_bwd_bf16_kernel<2>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
+      case 3: hipLaunchKernelGGL((ln_bwd_bf16_kernel<3>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
+      default: hipLaunchKernelGGL((ln_bwd_bf16_kernel<4>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
+    }
+    return hipGetLastError();
+  }
   switch (nc) {
     case 1: hipLaunchKernelGGL((ln_bwd_kernel<T, 1>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
     case 2: hipLaunchKernelGGL((ln_bwd_kernel<T, 2>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
