@@ -213,3 +213,24 @@ def test_bf16_bert_large_4_sequence_subset():
     sub = {"x": inp["x"][sel], "mask": inp["mask"][sel], "dy": dy[sel]}
     ref = run_oracle(cfg.with_(batch=2), sub, params)
     assert_bf16(lw, check_bf16(cfg, got, ref, rows=sel))
+
+
+def test_bf16_bert_base_8_uneven_sequence_subset():
+    """The uneven BERT-base share (8 layers, B32 x S512, valid lengths in
+    [256, 512]) on the full batch: partially masked 64-key blocks next to
+    unmasked ones, several 128-row blocks per head with the XCD grouping of
+    the attention grid.  dy is zero outside three sequences (the first, the
+    shortest and the last) and the oracle runs only those."""
+    cfg = synth.CONFIGS["bert_base_8_uneven"]
+    _say(f"case bf16 subset {cfg}")
+    inp = synth.make_inputs(cfg)
+    params = synth.make_params(cfg)
+    sel = np.zeros(cfg.batch, bool)
+    sel[[0, int(np.argmin(inp["lengths"])), cfg.batch - 1]] = True
+    dy = inp["dy"].copy()
+    dy[~sel] = 0.0
+    got = run_gpu(cfg, inp, params, dy=dy, saved=(0, 3))
+    lw = check_bf16_layerwise(cfg, inp, params, got, seqs=np.flatnonzero(sel))
+    sub = {"x": inp["x"][sel], "mask": inp["mask"][sel], "dy": dy[sel]}
+    ref = run_oracle(cfg.with_(batch=int(sel.sum())), sub, params)
+    assert_bf16(lw, check_bf16(cfg, got, ref, rows=sel))
