@@ -172,6 +172,18 @@ stage_status stage_trace_read(stage_t* s, int* launches, double* total_ms);
 int stage_site_count(void);
 const char* stage_site_name(int site); /* "" for an unknown site */
 
+/*
+ * Achievable dense bf16 MFMA throughput of the current device and the mean
+ * shader clock it held meanwhile: one work-group per compute unit, each
+ * wavefront issuing independent chains of 32x32x16 bf16 MFMAs on register
+ * operands for `iters` iterations (no memory traffic), timed with HIP events
+ * on hip_stream (NULL = default stream); the clock is the shader-cycle
+ * counter over the constant-rate counter.  Synchronous.  Writes TFLOP/s and
+ * GHz; EINVAL for null outputs or iters outside [1, 2^24], EHIP if the run
+ * fails.  Allocates and frees a few bytes of device memory per call.
+ */
+stage_status stage_mfma_peak(void* hip_stream, int iters, double* tflops, double* clock_ghz);
+
 /* Message describing the last failure on this handle ("" if none); with
  * s == NULL, the message of the last failed stage_init on this thread. */
 const char* stage_last_error(const stage_t* s);

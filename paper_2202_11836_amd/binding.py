@@ -30,7 +30,7 @@ ALLOC_STATUS_NAMES = {0: "OK", 1: "EINVAL", 2: "ENOFIT"}
 EXPORTED = ("alloc_coarse", "alloc_fine", "alloc_workloads", "stage_init", "stage_set_stream", "stage_forward", "stage_backward", "stage_param",
             "stage_grad", "stage_set_param", "stage_read", "stage_tensor_bytes",
             "stage_trace_site", "stage_trace_mask", "stage_trace_read", "stage_site_count",
-            "stage_site_name", "stage_device_bytes", "stage_memory_model",
+            "stage_site_name", "stage_device_bytes", "stage_memory_model", "stage_mfma_peak",
             "stage_last_error", "stage_destroy")
 
 _lib = None
@@ -99,6 +99,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.stage_memory_model.argtypes = [i32, i32, i32, i32, i32, i32, ctypes.POINTER(i64),
                                        ctypes.POINTER(i64)]
     lib.stage_memory_model.restype = i32
+    lib.stage_mfma_peak.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_double),
+                                    ctypes.POINTER(ctypes.c_double)]
+    lib.stage_mfma_peak.restype = i32
     dp, ip = ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)
     lib.alloc_coarse.argtypes = [i32, i32, dp, dp, ip, ip]
     lib.alloc_coarse.restype = i32
@@ -216,6 +219,15 @@ def stage_memory_model(hidden: int, heads: int, ffn: int, batch: int, seq: int, 
     _check(None, load_library().stage_memory_model(hidden, heads, ffn, batch, seq, dtype,
                                                    ctypes.byref(a), ctypes.byref(b)))
     return a.value, b.value
+
+
+def stage_mfma_peak(iters: int = 20000, stream=None):
+    """(TFLOP/s, GHz): achievable dense bf16 MFMA rate and the shader clock
+    held meanwhile, on the current device and stream."""
+    t, g = ctypes.c_double(0.0), ctypes.c_double(0.0)
+    st = stream if stream is not None else _current_stream()
+    _check(None, load_library().stage_mfma_peak(st, iters, ctypes.byref(t), ctypes.byref(g)))
+    return t.value, g.value
 
 
 def stage_last_error(handle) -> str:

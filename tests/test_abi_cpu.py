@@ -64,3 +64,17 @@ def _load_fresh(binding, path):
         binding.load_library(path)
     finally:
         binding._lib = saved
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="library not built (run __graft_entry__.build())")
+def test_mfma_peak_rejects_bad_arguments():
+    # argument checks come before any device call
+    lib = ctypes.CDLL(LIB)
+    t, g = ctypes.c_double(0.0), ctypes.c_double(0.0)
+    f = lib.stage_mfma_peak
+    f.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+                  ctypes.POINTER(ctypes.c_double)]
+    f.restype = ctypes.c_int
+    assert f(None, 0, ctypes.byref(t), ctypes.byref(g)) == 1
+    assert f(None, 1 << 25, ctypes.byref(t), ctypes.byref(g)) == 1
+    assert f(None, 100, None, ctypes.byref(g)) == 1

@@ -164,3 +164,16 @@ def test_stream_is_respected():
     side.synchronize()
     assert torch.equal(y, ref)
     st.close()
+
+
+def test_mfma_peak_measurement():
+    """The device's achievable dense bf16 MFMA rate and the clock it holds:
+    within the physical range of an MI355X (256 compute units, at most
+    2.4 GHz, 2516.6 TFLOP/s at that clock) and consistent with each other
+    (the rate cannot exceed what the measured clock allows)."""
+    import paper_2202_11836_amd as P
+    tf, ghz = P.stage_mfma_peak(4000)
+    print(f"case mfma peak: {tf:.1f} TFLOP/s at {ghz:.3f} GHz", flush=True)
+    assert 0.5 < ghz < 2.6
+    assert 200.0 < tf <= 2516.6 * 1.01
+    assert tf <= 2516.6 * ghz / 2.4 * 1.05
