@@ -92,6 +92,38 @@ typedef enum {
 stage_status stage_init(int L_stage, int hidden, int heads, int ffn, uint64_t seed,
                         stage_dtype dtype, void* hip_stream, stage_t** out);
 
+/*
+ * Create a stage that starts and ends at half-layer boundaries.  The layer
+ * allocator of section IV places discrete layers, whose count may exceed
+ * the number of encoder layers (the strong-scaling model of section VI-G
+ * counts several allocation units per encoder layer).  Here every encoder
+ * layer is two units, cut where a single tensor crosses in each direction:
+ *   unit 2j     attention half of layer j: QKV projection, attention, output
+ *               projection, residual add and first LayerNorm (X -> H1);
+ *   unit 2j + 1 feed-forward half of layer j: widening layer and GELU,
+ *               narrowing layer, residual add and second LayerNorm
+ *               (H1 -> Y; H1 is also the residual).
+ * The stage holds units [first_unit, first_unit + n_units): its layer l is
+ * global layer first_unit / 2 + l, and L_stage = (last unit) / 2 -
+ * first_unit / 2 + 1 layers are indexed in stage_param, stage_grad,
+ * stage_read, ...  Its input is X of its first unit's layer (H1 when
+ * first_unit is odd) and its output is that of its last unit.  Chaining the
+ * stages of a partition of [0, 2 L) computes the same function as one stage
+ * of L layers, except that on bf16 stages an H1 that crosses a stage
+ * boundary reaches the second LayerNorm rounded to bf16 (inside a stage it
+ * is added in fp32).  Weights are drawn as in stage_init with the global
+ * layer index, so a layer has the same weights in every stage that holds
+ * it; stage_init(L, ...) is stage_init_units(0, 2 L, ...).  Parameters,
+ * gradients and saved tensors of the absent half of a partial layer do not
+ * exist: stage_param, stage_grad, stage_set_param and stage_read return
+ * EINVAL for them (saved X, QKV, CTX belong to the attention half; H1, GD,
+ * G to the feed-forward half) and stage_tensor_bytes returns 0.
+ * EINVAL for first_unit < 0, n_units < 1, first_unit + n_units > 2^30 or
+ * dims stage_init rejects; otherwise as stage_init.
+ */
+stage_status stage_init_units(int first_unit, int n_units, int hidden, int heads, int ffn,
+                              uint64_t seed, stage_dtype dtype, void* hip_stream, stage_t** out);
+
 /* Change the stream later calls enqueue on. */
 stage_status stage_set_stream(stage_t* s, void* hip_stream);
 
@@ -129,6 +161,18 @@ stage_status stage_backward(stage_t* s, const void* dy, void* dx);
 stage_status stage_device_bytes(const stage_t* s, int64_t* bytes);
 stage_status stage_memory_model(int hidden, int heads, int ffn, int batch, int seq,
                                 stage_dtype dtype, int64_t* per_layer, int64_t* shared);
+/*
+ * The same per allocation unit (see stage_init_units): a stage of units
+ * [u0, u0 + n) holds shared + (its attention units) * attn_unit + (its
+ * feed-forward units) * ffn_unit bytes, and per_layer = attn_unit +
+ * ffn_unit.  The attention unit counts X, QKV, the score or log-sum-exp
+ * record, the context and the first LayerNorm's saved rows; the
+ * feed-forward unit counts its input H1, GELU'(U), G and the second
+ * LayerNorm's saved rows; each counts its own parameters and gradients.
+ */
+stage_status stage_memory_model_units(int hidden, int heads, int ffn, int batch, int seq,
+                                      stage_dtype dtype, int64_t* attn_unit, int64_t* ffn_unit,
+                                      int64_t* shared);
 
 /* Device pointer, element count and dtype of parameter `which` of `layer`. */
 stage_status stage_param(stage_t* s, int layer, int which, void** dev_ptr, int64_t* numel,

@@ -27,10 +27,12 @@ ALLOC_OK, ALLOC_EINVAL, ALLOC_ENOFIT = range(3)
 ALLOC_CT_PER_LAYER, ALLOC_CT_PER_DEVICE = 0, 1
 ALLOC_STATUS_NAMES = {0: "OK", 1: "EINVAL", 2: "ENOFIT"}
 
-EXPORTED = ("alloc_coarse", "alloc_fine", "alloc_workloads", "stage_init", "stage_set_stream", "stage_forward", "stage_backward", "stage_param",
+EXPORTED = ("alloc_coarse", "alloc_fine", "alloc_workloads", "stage_init", "stage_init_units",
+            "stage_set_stream", "stage_forward", "stage_backward", "stage_param",
             "stage_grad", "stage_set_param", "stage_read", "stage_tensor_bytes",
             "stage_trace_site", "stage_trace_mask", "stage_trace_read", "stage_site_count",
-            "stage_site_name", "stage_device_bytes", "stage_memory_model", "stage_mfma_peak",
+            "stage_site_name", "stage_device_bytes", "stage_memory_model",
+            "stage_memory_model_units", "stage_mfma_peak",
             "stage_last_error", "stage_destroy")
 
 _lib = None
@@ -64,6 +66,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     vp, i32, i64, u64, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_uint64, ctypes.c_size_t
     lib.stage_init.argtypes = [i32, i32, i32, i32, u64, i32, vp, ctypes.POINTER(vp)]
     lib.stage_init.restype = i32
+    lib.stage_init_units.argtypes = [i32, i32, i32, i32, i32, u64, i32, vp, ctypes.POINTER(vp)]
+    lib.stage_init_units.restype = i32
     lib.stage_set_stream.argtypes = [vp, vp]
     lib.stage_set_stream.restype = i32
     lib.stage_forward.argtypes = [vp, vp, vp, i32, i32, vp]
@@ -99,6 +103,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.stage_memory_model.argtypes = [i32, i32, i32, i32, i32, i32, ctypes.POINTER(i64),
                                        ctypes.POINTER(i64)]
     lib.stage_memory_model.restype = i32
+    lib.stage_memory_model_units.argtypes = [i32, i32, i32, i32, i32, i32, ctypes.POINTER(i64),
+                                             ctypes.POINTER(i64), ctypes.POINTER(i64)]
+    lib.stage_memory_model_units.restype = i32
     lib.stage_mfma_peak.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_double),
                                     ctypes.POINTER(ctypes.c_double)]
     lib.stage_mfma_peak.restype = i32
@@ -143,6 +150,18 @@ def stage_init(L: int, hidden: int, heads: int, ffn: int, seed: int, dtype: int,
                         stream if stream is not None else _current_stream(), ctypes.byref(out))
     if st != STAGE_OK:
         raise StageError(st, "stage_init: " + (lib.stage_last_error(None) or b"").decode())
+    return out
+
+
+def stage_init_units(first_unit: int, n_units: int, hidden: int, heads: int, ffn: int, seed: int,
+                     dtype: int, stream=None) -> ctypes.c_void_p:
+    lib = load_library()
+    out = ctypes.c_void_p()
+    st = lib.stage_init_units(first_unit, n_units, hidden, heads, ffn, seed, dtype,
+                              stream if stream is not None else _current_stream(),
+                              ctypes.byref(out))
+    if st != STAGE_OK:
+        raise StageError(st, "stage_init_units: " + (lib.stage_last_error(None) or b"").decode())
     return out
 
 
@@ -221,6 +240,15 @@ def stage_memory_model(hidden: int, heads: int, ffn: int, batch: int, seq: int, 
     return a.value, b.value
 
 
+def stage_memory_model_units(hidden: int, heads: int, ffn: int, batch: int, seq: int, dtype: int):
+    """(attn_unit, ffn_unit, shared) device bytes per half-layer unit."""
+    a, b, c = ctypes.c_int64(0), ctypes.c_int64(0), ctypes.c_int64(0)
+    _check(None, load_library().stage_memory_model_units(hidden, heads, ffn, batch, seq, dtype,
+                                                         ctypes.byref(a), ctypes.byref(b),
+                                                         ctypes.byref(c)))
+    return a.value, b.value, c.value
+
+
 def stage_mfma_peak(iters: int = 20000, stream=None):
     """(TFLOP/s, GHz): achievable dense bf16 MFMA rate and the shader clock
     held meanwhile, on the current device and stream."""
@@ -245,16 +273,26 @@ def stage_destroy(handle) -> None:
 # ---------------------------------------------------------------------------
 
 class Stage:
-    """One stage of L encoder layers on the current GPU."""
+    """One stage of L encoder layers on the current GPU, or, with
+    first_unit / n_units, of the half-layer units [first_unit, first_unit +
+    n_units) (unit 2j: attention half of layer j, unit 2j+1: its
+    feed-forward half; L is then the number of layers they touch)."""
 
-    def __init__(self, L: int, hidden: int, heads: int, ffn: int, seed: int = 0,
-                 dtype: str = "bf16"):
+    def __init__(self, L: Optional[int], hidden: int, heads: int, ffn: int, seed: int = 0,
+                 dtype: str = "bf16", first_unit: int = 0, n_units: Optional[int] = None):
         import torch
-        self.L, self.hidden, self.heads, self.ffn = L, hidden, heads, ffn
+        self.hidden, self.heads, self.ffn = hidden, heads, ffn
         self.dtype_name = dtype
         self.code = STAGE_BF16 if dtype == "bf16" else STAGE_F32
         self.torch_dtype = torch.bfloat16 if dtype == "bf16" else torch.float32
-        self.handle = stage_init(L, hidden, heads, ffn, seed, self.code)
+        if n_units is None:
+            self.first_unit, self.n_units = 0, 2 * L
+            self.handle = stage_init(L, hidden, heads, ffn, seed, self.code)
+        else:
+            self.first_unit, self.n_units = first_unit, n_units
+            self.handle = stage_init_units(first_unit, n_units, hidden, heads, ffn, seed, self.code)
+            L = (first_unit + n_units - 1) // 2 - first_unit // 2 + 1
+        self.L = L
 
     def _sync_stream(self):
         stage_set_stream(self.handle, _current_stream())

@@ -91,6 +91,10 @@ bool is_matrix(int which) {
   return which == STAGE_W_QKV || which == STAGE_W_O || which == STAGE_W_1 || which == STAGE_W_2;
 }
 
+// Parameters 0 .. STAGE_BE1 belong to the attention half of a layer, the
+// rest to its feed-forward half.
+bool is_attn_param(int which) { return which <= STAGE_BE1; }
+
 struct Saved {
   void* X = nullptr;     // layer input [T, h]
   void* QKV = nullptr;   // [T, 3h]
@@ -110,6 +114,14 @@ struct Saved {
 
 struct stage {
   int L = 0, h = 0, H = 0, f = 0;
+  // Allocation units (two per encoder layer): unit 2j is the attention half
+  // of global layer j (X -> H1), unit 2j+1 its feed-forward half (H1 -> Y).
+  // The stage holds units [2 l0 + ffn_first, ...); local layer l is global
+  // layer l0 + l.  ffn_first: local layer 0 has only its feed-forward half
+  // (the stage input is H1); attn_last: local layer L-1 has only its
+  // attention half (the stage output is H1).
+  int l0 = 0;
+  bool ffn_first = false, attn_last = false;
   stage_dtype dtype = STAGE_F32;
   size_t esz = 4;
   hipStream_t stream = nullptr;
@@ -165,6 +177,13 @@ namespace {
 
 // Message of the last failed stage_init on this thread (no handle exists).
 thread_local std::string g_init_err;
+
+// Which halves of local layer l the stage holds.
+bool has_attn(const stage_t* s, int l) { return !(l == 0 && s->ffn_first); }
+bool has_ffn(const stage_t* s, int l) { return !(l == s->L - 1 && s->attn_last); }
+bool has_param(const stage_t* s, int l, int which) {
+  return is_attn_param(which) ? has_attn(s, l) : has_ffn(s, l);
+}
 
 stage_status fail(stage_t* s, stage_status st, const std::string& msg) {
   if (s) s->err = msg;
@@ -287,13 +306,19 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
   auto A = [&](void** p, size_t bytes) { return dev_alloc(s, s->act_allocs, p, bytes); };
   stage_status st;
   s->saved.resize(s->L);
+  // The attention half of a layer saves X, QKV, P, lse, C, xhat1, rstd1;
+  // the feed-forward half saves its input H1, GELU'(U), G, xhat2, rstd2.
   for (int l = 0; l < s->L; ++l) {
     Saved& v = s->saved[l];
-    if ((st = A(&v.X, T * h * e)) || (st = A(&v.QKV, T * 3 * h * e)) ||
-        (st = A(&v.P, BSS * e)) || (st = A((void**)&v.lse, BHS * 4)) || (st = A(&v.C, T * h * e)) || (st = A(&v.xhat1, T * h * e)) ||
-        (st = A((void**)&v.rstd1, T * 4)) || (st = A(&v.H1, T * h * e)) ||
-        (st = A(&v.Gd, T * f * e)) || (st = A(&v.G, T * f * e)) ||
-        (st = A(&v.xhat2, T * h * e)) || (st = A((void**)&v.rstd2, T * 4)))
+    if (has_attn(s, l) &&
+        ((st = A(&v.X, T * h * e)) || (st = A(&v.QKV, T * 3 * h * e)) ||
+         (st = A(&v.P, BSS * e)) || (st = A((void**)&v.lse, BHS * 4)) ||
+         (st = A(&v.C, T * h * e)) || (st = A(&v.xhat1, T * h * e)) ||
+         (st = A((void**)&v.rstd1, T * 4))))
+      return st;
+    if (has_ffn(s, l) &&
+        ((st = A(&v.H1, T * h * e)) || (st = A(&v.Gd, T * f * e)) || (st = A(&v.G, T * f * e)) ||
+         (st = A(&v.xhat2, T * h * e)) || (st = A((void**)&v.rstd2, T * 4))))
       return st;
   }
   if ((st = A((void**)&s->mask, T)) || (st = A((void**)&s->tmp, T * h * 4)) ||
@@ -395,59 +420,73 @@ stage_status forward_impl(stage_t* s, const T* x, T* y) {
   const int BH = B * H;
   hipStream_t st = s->stream;
   const float scale = 1.0f / sqrtf((float)HEAD_DIM);
-  HIPCK(hipMemcpyAsync(s->saved[0].X, x, (size_t)Tn * h * sizeof(T), hipMemcpyDeviceToDevice, st));
-  if (std::is_same<T, bf16_t>::value) SITE(KEXT, key_extent(s->mask, B, S, s->kext, st));
+  // The stage input is X of local layer 0, or its H1 when that layer holds
+  // only its feed-forward half.
+  HIPCK(hipMemcpyAsync(s->ffn_first ? s->saved[0].H1 : s->saved[0].X, x, (size_t)Tn * h * sizeof(T),
+                       hipMemcpyDeviceToDevice, st));
+  if (std::is_same<T, bf16_t>::value && (s->L > 1 || !s->ffn_first))
+    SITE(KEXT, key_extent(s->mask, B, S, s->kext, st));
   for (int l = 0; l < s->L; ++l) {
     Saved& v = s->saved[l];
     auto& p = s->param[l];
-    const T* X = (const T*)v.X;
-    T* QKV = (T*)v.QKV;
-    // QKV = X W_qkv^T + b_qkv
-    {
-      GemmArgs g = gemm_args(X, h, p[STAGE_W_QKV], h, QKV, 3 * h, Tn, 3 * h, h);
-      g.bias = (const float*)p[STAGE_B_QKV];
-      SITE(QKV_FWD, Gemm<T>::run(g, true, true, EPI_STORE, false, 1, st));
-    }
-    if constexpr (std::is_same<T, bf16_t>::value) {
-      // Fused attention: softmax(Q K^T / 8) V per (batch, head), P stays on chip.
-      AttnArgs aa = attn_args(s, (const bf16_t*)QKV, (bf16_t*)v.C, v.lse);
-      SITE(ATTN_FWD, attn_forward(aa, st));
-    } else {
-    // scores[b, j] = Q_bj K_bj^T  (fp32)
-    {
-      GemmArgs g = gemm_args(QKV, 3 * h, QKV + h, 3 * h, s->scores, S, S, S, HEAD_DIM);
-      g.zdiv = H;
-      g.sA1 = g.sB1 = (int64_t)S * 3 * h;
-      g.sA2 = g.sB2 = HEAD_DIM;
-      g.sC1 = (int64_t)H * S * S;
-      g.sC2 = (int64_t)S * S;
-      SITE(SCORES_FWD, Gemm<T>::run(g, true, true, EPI_STORE, true, BH, st));
-    }
-    SITE(SOFTMAX_FWD, softmax_fwd<T>(s->scores, s->mask, (T*)v.P, BH, H, S, S, scale, st));
-    // C[b, :, j] = P_bj V_bj
-    {
-      GemmArgs g = gemm_args(v.P, S, QKV + 2 * h, 3 * h, v.C, h, S, HEAD_DIM, S);
-      g.zdiv = H;
-      g.sA1 = (int64_t)H * S * S;
-      g.sA2 = (int64_t)S * S;
-      g.sB1 = (int64_t)S * 3 * h;
-      g.sB2 = HEAD_DIM;
-      g.sC1 = (int64_t)S * h;
-      g.sC2 = HEAD_DIM;
-      SITE(CTX_FWD, Gemm<T>::run(g, true, false, EPI_STORE, false, BH, st));
-    }
-    }
-    // tmp = C W_o^T (fp32);  H1 = LN(X + tmp + b_o)
-    {
-      GemmArgs g = gemm_args(v.C, h, p[STAGE_W_O], h, s->tmp, h, Tn, h, h);
-      SITE(OUT_FWD, Gemm<T>::run(g, true, true, EPI_STORE, true, 1, st));
-    }
-    // For bf16 stages H1 is also written in fp32: it is the residual of the
-    // second LayerNorm, so its rounding to bf16 stays out of Y.
-    float* h1_32 = std::is_same<T, float>::value ? nullptr : s->h1f;
-    SITE(LN1_FWD, add_ln_fwd<T, float, T>(s->tmp, (const float*)p[STAGE_B_O], X,
-                                   (const float*)p[STAGE_G1], (const float*)p[STAGE_BE1],
-                                   (T*)v.H1, h1_32, (T*)v.xhat1, v.rstd1, Tn, h, st));
+    // For bf16 stages H1 is also written in fp32 when this stage computes
+    // it: it is the residual of the second LayerNorm, so its rounding to
+    // bf16 stays out of Y.  (A stage that starts at a feed-forward half
+    // receives H1 in bf16, as the previous stage's output.)
+    float* h1_32 = (std::is_same<T, float>::value || !has_attn(s, l)) ? nullptr : s->h1f;
+    if (has_attn(s, l)) {
+      const T* X = (const T*)v.X;
+      T* QKV = (T*)v.QKV;
+      // QKV = X W_qkv^T + b_qkv
+      {
+        GemmArgs g = gemm_args(X, h, p[STAGE_W_QKV], h, QKV, 3 * h, Tn, 3 * h, h);
+        g.bias = (const float*)p[STAGE_B_QKV];
+        SITE(QKV_FWD, Gemm<T>::run(g, true, true, EPI_STORE, false, 1, st));
+      }
+      if constexpr (std::is_same<T, bf16_t>::value) {
+        // Fused attention: softmax(Q K^T / 8) V per (batch, head), P stays on chip.
+        AttnArgs aa = attn_args(s, (const bf16_t*)QKV, (bf16_t*)v.C, v.lse);
+        SITE(ATTN_FWD, attn_forward(aa, st));
+      } else {
+      // scores[b, j] = Q_bj K_bj^T  (fp32)
+      {
+        GemmArgs g = gemm_args(QKV, 3 * h, QKV + h, 3 * h, s->scores, S, S, S, HEAD_DIM);
+        g.zdiv = H;
+        g.sA1 = g.sB1 = (int64_t)S * 3 * h;
+        g.sA2 = g.sB2 = HEAD_DIM;
+        g.sC1 = (int64_t)H * S * S;
+        g.sC2 = (int64_t)S * S;
+        SITE(SCORES_FWD, Gemm<T>::run(g, true, true, EPI_STORE, true, BH, st));
+      }
+      SITE(SOFTMAX_FWD, softmax_fwd<T>(s->scores, s->mask, (T*)v.P, BH, H, S, S, scale, st));
+      // C[b, :, j] = P_bj V_bj
+      {
+        GemmArgs g = gemm_args(v.P, S, QKV + 2 * h, 3 * h, v.C, h, S, HEAD_DIM, S);
+        g.zdiv = H;
+        g.sA1 = (int64_t)H * S * S;
+        g.sA2 = (int64_t)S * S;
+        g.sB1 = (int64_t)S * 3 * h;
+        g.sB2 = HEAD_DIM;
+        g.sC1 = (int64_t)S * h;
+        g.sC2 = HEAD_DIM;
+        SITE(CTX_FWD, Gemm<T>::run(g, true, false, EPI_STORE, false, BH, st));
+      }
+      }
+      // tmp = C W_o^T (fp32);  H1 = LN(X + tmp + b_o)
+      {
+        GemmArgs g = gemm_args(v.C, h, p[STAGE_W_O], h, s->tmp, h, Tn, h, h);
+        SITE(OUT_FWD, Gemm<T>::run(g, true, true, EPI_STORE, true, 1, st));
+      }
+      // The last layer of a stage that ends at an attention half writes H1
+      // straight to the stage output.
+      const bool to_out = !has_ffn(s, l);
+      if (to_out) h1_32 = nullptr;
+      SITE(LN1_FWD, add_ln_fwd<T, float, T>(s->tmp, (const float*)p[STAGE_B_O], X,
+                                     (const float*)p[STAGE_G1], (const float*)p[STAGE_BE1],
+                                     to_out ? y : (T*)v.H1, h1_32, (T*)v.xhat1, v.rstd1, Tn, h,
+                                     st));
+      if (to_out) break;
+    }  // attention half
     // U = H1 W_1^T + b_1;  G = GELU(U) and GELU'(U) (kept for the backward)
     {
       GemmArgs g = gemm_args(v.H1, h, p[STAGE_W_1], h, v.G, f, Tn, f, h);
@@ -520,51 +559,67 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
     const void* Wo = p[STAGE_W_O];
     const void* W1 = p[STAGE_W_1];
     const void* W2 = p[STAGE_W_2];
+    const bool attn = has_attn(s, l), ffn = has_ffn(s, l);
     if (kBF) {
-      const TransposeJob jobs[4] = {{(const bf16_t*)Wq, (bf16_t*)s->wt_qkv, 3 * h, h, 0},
-                                    {(const bf16_t*)Wo, (bf16_t*)s->wt_o, h, h, 0},
-                                    {(const bf16_t*)W1, (bf16_t*)s->wt_1, f, h, 0},
-                                    {(const bf16_t*)W2, (bf16_t*)s->wt_2, h, f, 0}};
-      SITE(WT, transpose_bf16(jobs, 4, st));
+      TransposeJob jobs[4];
+      int nj = 0;
+      if (attn) {
+        jobs[nj++] = {(const bf16_t*)Wq, (bf16_t*)s->wt_qkv, 3 * h, h, 0};
+        jobs[nj++] = {(const bf16_t*)Wo, (bf16_t*)s->wt_o, h, h, 0};
+      }
+      if (ffn) {
+        jobs[nj++] = {(const bf16_t*)W1, (bf16_t*)s->wt_1, f, h, 0};
+        jobs[nj++] = {(const bf16_t*)W2, (bf16_t*)s->wt_2, h, f, 0};
+      }
+      SITE(WT, transpose_bf16(jobs, nj, st));
       Wq = s->wt_qkv;
       Wo = s->wt_o;
       W1 = s->wt_1;
       W2 = s->wt_2;
     }
-    // Y = LN(Z2): dZ2, dgamma2, dbeta2, and db_2 = sum_t dZ2
-    if ((r = ln_backward<T>(s, SITE_LN2_BWD, SITE_LN2_RED, dYcur, (const T*)v.xhat2, v.rstd2, (const float*)p[STAGE_G2], dZ2,
-                            gr[STAGE_G2], gr[STAGE_BE2], gr[STAGE_B_2])))
-      return r;
-    // dW_2 = dZ2^T G
-    if ((r = wgrad<T>(s, SITE_W2_WGRAD, SITE_W2_RED, dZ2, h, (const T*)v.G, f, h, f, Tn, gr[STAGE_W_2]))) return r;
-    // dU = (dZ2 W_2) * GELU'(U)
-    {
-      GemmArgs g = gemm_args(dZ2, h, W2, kBF ? h : f, dU, f, Tn, f, h);
-      g.aux = v.Gd;
-      g.ldaux = f;
-      if (kBF) {  // db_1 = column sums of dU, accumulated in the epilogue
-        g.tile = 1;
-        g.colpart = s->colpart_ffn;
+    // Gradient reaching H1: computed by the feed-forward half, or the
+    // incoming dy when the stage ends at this layer's attention half.
+    const T* dH1in = dYcur;
+    if (ffn) {
+      // Y = LN(Z2): dZ2, dgamma2, dbeta2, and db_2 = sum_t dZ2
+      if ((r = ln_backward<T>(s, SITE_LN2_BWD, SITE_LN2_RED, dYcur, (const T*)v.xhat2, v.rstd2, (const float*)p[STAGE_G2], dZ2,
+                              gr[STAGE_G2], gr[STAGE_BE2], gr[STAGE_B_2])))
+        return r;
+      // dW_2 = dZ2^T G
+      if ((r = wgrad<T>(s, SITE_W2_WGRAD, SITE_W2_RED, dZ2, h, (const T*)v.G, f, h, f, Tn, gr[STAGE_W_2]))) return r;
+      // dU = (dZ2 W_2) * GELU'(U)
+      {
+        GemmArgs g = gemm_args(dZ2, h, W2, kBF ? h : f, dU, f, Tn, f, h);
+        g.aux = v.Gd;
+        g.ldaux = f;
+        if (kBF) {  // db_1 = column sums of dU, accumulated in the epilogue
+          g.tile = 1;
+          g.colpart = s->colpart_ffn;
+        }
+        SITE(FFN2_DGRAD, Gemm<T>::run(g, true, kBF, EPI_MUL, false, 1, st));
       }
-      SITE(FFN2_DGRAD, Gemm<T>::run(g, true, kBF, EPI_MUL, false, 1, st));
-    }
-    if (kBF) {
-      float* outs[1] = {gr[STAGE_B_1]};
-      SITE(B1_RED, col_reduce(s->colpart_ffn, (Tn + 127) / 128, 1, f, outs, st));
-    } else if ((r = col_sum<T>(s, SITE_B1_SUM, SITE_B1_RED, dU, f, gr[STAGE_B_1]))) {
-      return r;
-    }
-    // dW_1 = dU^T H1
-    if ((r = wgrad<T>(s, SITE_W1_WGRAD, SITE_W1_RED, dU, f, (const T*)v.H1, h, f, h, Tn, gr[STAGE_W_1]))) return r;
-    // dH1 = dZ2 + dU W_1
-    {
-      GemmArgs g = gemm_args(dU, f, W1, kBF ? f : h, dH1, h, Tn, h, f);
-      g.aux = dZ2;
-      g.ldaux = h;
-      SITE(FFN1_DGRAD, Gemm<T>::run(g, true, kBF, EPI_RESID, false, 1, st));
-    }
+      if (kBF) {
+        float* outs[1] = {gr[STAGE_B_1]};
+        SITE(B1_RED, col_reduce(s->colpart_ffn, (Tn + 127) / 128, 1, f, outs, st));
+      } else if ((r = col_sum<T>(s, SITE_B1_SUM, SITE_B1_RED, dU, f, gr[STAGE_B_1]))) {
+        return r;
+      }
+      // dW_1 = dU^T H1
+      if ((r = wgrad<T>(s, SITE_W1_WGRAD, SITE_W1_RED, dU, f, (const T*)v.H1, h, f, h, Tn, gr[STAGE_W_1]))) return r;
+      // dH1 = dZ2 + dU W_1 (the stage's dx when it starts at this layer's
+      // feed-forward half)
+      T* dH1out = attn ? dH1 : dx;
+      {
+        GemmArgs g = gemm_args(dU, f, W1, kBF ? f : h, dH1out, h, Tn, h, f);
+        g.aux = dZ2;
+        g.ldaux = h;
+        SITE(FFN1_DGRAD, Gemm<T>::run(g, true, kBF, EPI_RESID, false, 1, st));
+      }
+      dH1in = dH1out;
+    }  // feed-forward half
+    if (!attn) break;
     // H1 = LN(Z1): dZ1, dgamma1, dbeta1, db_o
-    if ((r = ln_backward<T>(s, SITE_LN1_BWD, SITE_LN1_RED, dH1, (const T*)v.xhat1, v.rstd1, (const float*)p[STAGE_G1], dZ1,
+    if ((r = ln_backward<T>(s, SITE_LN1_BWD, SITE_LN1_RED, dH1in, (const T*)v.xhat1, v.rstd1, (const float*)p[STAGE_G1], dZ1,
                             gr[STAGE_G1], gr[STAGE_BE1], gr[STAGE_B_O])))
       return r;
     // dW_o = dZ1^T C
@@ -652,61 +707,49 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
   return STAGE_OK;
 }
 
-stage_status check_layer(stage_t* s, int layer, int which, int nwhich) {
-  if (!s) return STAGE_EINVAL;
-  if (layer < 0 || layer >= s->L) return fail(s, STAGE_EINVAL, "layer index out of range");
-  if (which < 0 || which >= nwhich) return fail(s, STAGE_EINVAL, "tensor index out of range");
-  return STAGE_OK;
+bool valid_dims(int hidden, int heads, int ffn, stage_dtype dtype) {
+  return hidden >= 64 && hidden % 64 == 0 && hidden <= 2048 && heads >= 1 && hidden % heads == 0 &&
+         hidden / heads == HEAD_DIM && ffn >= 64 && ffn % 64 == 0 &&
+         (dtype == STAGE_F32 || dtype == STAGE_BF16);
 }
 
-}  // namespace
-
-// ===========================================================================
-// C ABI
-// ===========================================================================
-extern "C" {
-
-stage_status stage_init(int L, int hidden, int heads, int ffn, uint64_t seed, stage_dtype dtype,
-                        void* hip_stream, stage_t** out) {
-  g_init_err.clear();
-  if (!out) {
-    g_init_err = "null out";
-    return STAGE_EINVAL;
-  }
-  *out = nullptr;
-  if (L < 1 || hidden < 64 || hidden % 64 || hidden > 2048 || heads < 1 || hidden % heads ||
-      hidden / heads != HEAD_DIM || ffn < 64 || ffn % 64 ||
-      (dtype != STAGE_F32 && dtype != STAGE_BF16)) {
-    g_init_err = "invalid dims: need L >= 1, hidden a multiple of 64 and <= 2048, "
-                 "hidden / heads == 64, ffn a multiple of 64";
-    return STAGE_EINVAL;
-  }
-  stage_t* s = new (std::nothrow) stage_t();
-  if (!s) return STAGE_ENOMEM;
-  s->L = L;
+// Shape of a stage holding units [first_unit, first_unit + n_units).
+void set_units(stage_t* s, int first_unit, int n_units, int hidden, int heads, int ffn,
+               stage_dtype dtype) {
+  const int last = first_unit + n_units - 1;
+  s->l0 = first_unit / 2;
+  s->L = last / 2 - s->l0 + 1;
+  s->ffn_first = (first_unit & 1) != 0;
+  s->attn_last = (last & 1) == 0;
   s->h = hidden;
   s->H = heads;
   s->f = ffn;
   s->dtype = dtype;
   s->esz = dtype == STAGE_BF16 ? 2 : 4;
-  s->stream = (hipStream_t)hip_stream;
-  s->param.resize(L);
-  s->grad.resize(L);
-  for (int l = 0; l < L; ++l) {
+}
+
+// Allocates and initialises the parameters and gradients of the halves the
+// stage holds (a dry-run stage only counts the bytes).  Weights of global
+// layer j are drawn from keys that depend on (seed, j, tensor) only, so a
+// layer has the same weights in every stage that holds it.
+stage_status build_params(stage_t* s, uint64_t seed) {
+  s->param.assign(s->L, {});
+  s->grad.assign(s->L, {});
+  for (int l = 0; l < s->L; ++l) {
+    const uint64_t gl = (uint64_t)(s->l0 + l);
     for (int w = 0; w < STAGE_NPARAM; ++w) {
-      int64_t n = param_numel(s, w);
+      s->param[l][w] = nullptr;
+      s->grad[l][w] = nullptr;
+      if (!has_param(s, l, w)) continue;
+      const int64_t n = param_numel(s, w);
       stage_status st = dev_alloc(s, s->allocs, &s->param[l][w], n * param_esz(s, w));
       if (!st) st = dev_alloc(s, s->allocs, (void**)&s->grad[l][w], n * 4);
-      if (st) {
-        g_init_err = s->err;
-        for (void* p : s->allocs) (void)hipFree(p);
-        delete s;
-        return st;
-      }
+      if (st) return st;
+      if (s->dry_run) continue;
       const int blocks = (int)((n + 255) / 256);
       if (is_matrix(w)) {
-        uint64_t key = splitmix64_mix(seed ^ ((uint64_t)(l * STAGE_NPARAM + w + 1) * GOLDEN));
-        if (dtype == STAGE_BF16)
+        uint64_t key = splitmix64_mix(seed ^ ((gl * STAGE_NPARAM + w + 1) * GOLDEN));
+        if (s->dtype == STAGE_BF16)
           hipLaunchKernelGGL(init_normal_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s->stream,
                              (bf16_t*)s->param[l][w], n, key, 0.02);
         else
@@ -721,13 +764,85 @@ stage_status stage_init(int L, int hidden, int heads, int ffn, uint64_t seed, st
                          0.0f);
     }
   }
+  if (s->dry_run) return STAGE_OK;
   hipError_t e = hipGetLastError();
   if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
-  if (e != hipSuccess) {
-    g_init_err = std::string("initialisation kernels: ") + hipGetErrorString(e);
+  if (e != hipSuccess)
+    return fail(s, STAGE_EHIP, std::string("initialisation kernels: ") + hipGetErrorString(e));
+  return STAGE_OK;
+}
+
+// Device bytes of a dry-run stage of units [first_unit, first_unit +
+// n_units) after a forward of batch x seq tokens; -1 on failure.
+int64_t dry_bytes(int first_unit, int n_units, int hidden, int heads, int ffn, int batch, int seq,
+                  stage_dtype dtype) {
+  stage_t d;
+  d.dry_run = true;
+  set_units(&d, first_unit, n_units, hidden, heads, ffn, dtype);
+  if (build_params(&d, 0) != STAGE_OK || ensure_activations(&d, batch, seq) != STAGE_OK) return -1;
+  return d.bytes_param + d.bytes_act;
+}
+
+stage_status check_layer(stage_t* s, int layer, int which, int nwhich) {
+  if (!s) return STAGE_EINVAL;
+  if (layer < 0 || layer >= s->L) return fail(s, STAGE_EINVAL, "layer index out of range");
+  if (which < 0 || which >= nwhich) return fail(s, STAGE_EINVAL, "tensor index out of range");
+  return STAGE_OK;
+}
+
+// A parameter (or its gradient) of a half-layer the stage holds.
+stage_status check_param(stage_t* s, int layer, int which) {
+  stage_status st = check_layer(s, layer, which, STAGE_NPARAM);
+  if (st) return st;
+  if (!has_param(s, layer, which))
+    return fail(s, STAGE_EINVAL, "the stage does not hold this half of the layer");
+  return STAGE_OK;
+}
+
+}  // namespace
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+extern "C" {
+
+stage_status stage_init(int L, int hidden, int heads, int ffn, uint64_t seed, stage_dtype dtype,
+                        void* hip_stream, stage_t** out) {
+  if (L < 1 || L > (1 << 29)) {
+    g_init_err = "invalid dims: need 1 <= L <= 2^29";
+    if (out) *out = nullptr;
+    return STAGE_EINVAL;
+  }
+  return stage_init_units(0, 2 * L, hidden, heads, ffn, seed, dtype, hip_stream, out);
+}
+
+stage_status stage_init_units(int first_unit, int n_units, int hidden, int heads, int ffn,
+                              uint64_t seed, stage_dtype dtype, void* hip_stream, stage_t** out) {
+  g_init_err.clear();
+  if (!out) {
+    g_init_err = "null out";
+    return STAGE_EINVAL;
+  }
+  *out = nullptr;
+  if (first_unit < 0 || n_units < 1 || n_units > (1 << 30) - first_unit) {
+    g_init_err = "invalid units: need first_unit >= 0, n_units >= 1, first_unit + n_units <= 2^30";
+    return STAGE_EINVAL;
+  }
+  if (!valid_dims(hidden, heads, ffn, dtype)) {
+    g_init_err = "invalid dims: need hidden a multiple of 64 and <= 2048, "
+                 "hidden / heads == 64, ffn a multiple of 64";
+    return STAGE_EINVAL;
+  }
+  stage_t* s = new (std::nothrow) stage_t();
+  if (!s) return STAGE_ENOMEM;
+  set_units(s, first_unit, n_units, hidden, heads, ffn, dtype);
+  s->stream = (hipStream_t)hip_stream;
+  stage_status st = build_params(s, seed);
+  if (st) {
+    g_init_err = s->err;
     for (void* p : s->allocs) (void)hipFree(p);
     delete s;
-    return STAGE_EHIP;
+    return st;
   }
   *out = s;
   return STAGE_OK;
@@ -786,6 +901,7 @@ stage_status stage_backward(stage_t* s, const void* dy, void* dx) {
   if (T == 0) {
     for (int l = 0; l < s->L; ++l)
       for (int w = 0; w < STAGE_NPARAM; ++w) {
+        if (!has_param(s, l, w)) continue;
         int64_t n = param_numel(s, w);
         hipLaunchKernelGGL(fill_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
                            s->stream, s->grad[l][w], n, 0.0f);
@@ -799,7 +915,7 @@ stage_status stage_backward(stage_t* s, const void* dy, void* dx) {
 
 stage_status stage_param(stage_t* s, int layer, int which, void** dev_ptr, int64_t* numel,
                          stage_dtype* dtype) {
-  stage_status st = check_layer(s, layer, which, STAGE_NPARAM);
+  stage_status st = check_param(s, layer, which);
   if (st) return st;
   if (dev_ptr) *dev_ptr = s->param[layer][which];
   if (numel) *numel = param_numel(s, which);
@@ -808,7 +924,7 @@ stage_status stage_param(stage_t* s, int layer, int which, void** dev_ptr, int64
 }
 
 stage_status stage_grad(stage_t* s, int layer, int which, float** dev_ptr, int64_t* numel) {
-  stage_status st = check_layer(s, layer, which, STAGE_NPARAM);
+  stage_status st = check_param(s, layer, which);
   if (st) return st;
   if (dev_ptr) *dev_ptr = s->grad[layer][which];
   if (numel) *numel = param_numel(s, which);
@@ -816,7 +932,7 @@ stage_status stage_grad(stage_t* s, int layer, int which, float** dev_ptr, int64
 }
 
 stage_status stage_set_param(stage_t* s, int layer, int which, const void* src, size_t bytes) {
-  stage_status st = check_layer(s, layer, which, STAGE_NPARAM);
+  stage_status st = check_param(s, layer, which);
   if (st) return st;
   if (!src) return fail(s, STAGE_EINVAL, "null src");
   size_t want = (size_t)param_numel(s, which) * param_esz(s, which);
@@ -830,23 +946,27 @@ static void* saved_ptr(stage_t* s, int layer, int which, size_t* bytes) {
   const int64_t T = (int64_t)s->B * s->S;
   const Saved& v = s->saved[layer];
   const size_t e = s->esz;
-  switch (which) {
-    case STAGE_SAVED_X: *bytes = T * s->h * e; return v.X;
-    case STAGE_SAVED_QKV: *bytes = T * 3 * s->h * e; return v.QKV;
-    case STAGE_SAVED_CTX: *bytes = T * s->h * e; return v.C;
-    case STAGE_SAVED_H1: *bytes = T * s->h * e; return v.H1;
-    case STAGE_SAVED_GD: *bytes = T * s->f * e; return v.Gd;
-    case STAGE_SAVED_G: *bytes = T * s->f * e; return v.G;
-  }
+  // Tensors of a half-layer the stage does not hold have no storage (H1 of
+  // a layer whose feed-forward half is absent went to the stage output).
+  const bool attn = has_attn(s, layer), ffn = has_ffn(s, layer);
   *bytes = 0;
+  switch (which) {
+    case STAGE_SAVED_X: if (attn) *bytes = T * s->h * e; return attn ? v.X : nullptr;
+    case STAGE_SAVED_QKV: if (attn) *bytes = T * 3 * s->h * e; return attn ? v.QKV : nullptr;
+    case STAGE_SAVED_CTX: if (attn) *bytes = T * s->h * e; return attn ? v.C : nullptr;
+    case STAGE_SAVED_H1: if (ffn) *bytes = T * s->h * e; return ffn ? v.H1 : nullptr;
+    case STAGE_SAVED_GD: if (ffn) *bytes = T * s->f * e; return ffn ? v.Gd : nullptr;
+    case STAGE_SAVED_G: if (ffn) *bytes = T * s->f * e; return ffn ? v.G : nullptr;
+  }
   return nullptr;
 }
 
 size_t stage_tensor_bytes(stage_t* s, int kind, int layer, int which) {
   if (!s || layer < 0 || layer >= s->L) return 0;
-  if (kind == 0 && which >= 0 && which < STAGE_NPARAM)
-    return (size_t)param_numel(s, which) * param_esz(s, which);
-  if (kind == 1 && which >= 0 && which < STAGE_NPARAM) return (size_t)param_numel(s, which) * 4;
+  if ((kind == 0 || kind == 1) && (which < 0 || which >= STAGE_NPARAM || !has_param(s, layer, which)))
+    return 0;
+  if (kind == 0) return (size_t)param_numel(s, which) * param_esz(s, which);
+  if (kind == 1) return (size_t)param_numel(s, which) * 4;
   if (kind == 2 && which >= 0 && which < STAGE_NSAVED && (int)s->saved.size() == s->L) {
     size_t b;
     saved_ptr(s, layer, which, &b);
@@ -861,7 +981,7 @@ stage_status stage_read(stage_t* s, int kind, int layer, int which, void* dst, s
   const void* src = nullptr;
   size_t want = 0;
   if (kind == 0 || kind == 1) {
-    stage_status st = check_layer(s, layer, which, STAGE_NPARAM);
+    stage_status st = check_param(s, layer, which);
     if (st) return st;
     src = kind == 0 ? s->param[layer][which] : (const void*)s->grad[layer][which];
     want = (size_t)param_numel(s, which) * (kind == 0 ? param_esz(s, which) : 4);
@@ -870,6 +990,7 @@ stage_status stage_read(stage_t* s, int kind, int layer, int which, void* dst, s
     if (st) return st;
     if ((int)s->saved.size() != s->L) return fail(s, STAGE_ESTATE, "no saved activations");
     src = saved_ptr(s, layer, which, &want);
+    if (!src) return fail(s, STAGE_EINVAL, "the stage does not hold this half of the layer");
   } else {
     return fail(s, STAGE_EINVAL, "kind must be 0 (param), 1 (grad) or 2 (saved)");
   }
@@ -919,37 +1040,31 @@ stage_status stage_device_bytes(const stage_t* s, int64_t* bytes) {
 
 stage_status stage_memory_model(int hidden, int heads, int ffn, int batch, int seq,
                                 stage_dtype dtype, int64_t* per_layer, int64_t* shared) {
+  int64_t attn, ffn_b, sh;
+  stage_status st = stage_memory_model_units(hidden, heads, ffn, batch, seq, dtype, &attn, &ffn_b, &sh);
+  if (st) return st;
   if (!per_layer || !shared) return STAGE_EINVAL;
-  if (hidden < 64 || hidden % 64 || hidden > 2048 || heads < 1 || hidden % heads ||
-      hidden / heads != HEAD_DIM || ffn < 64 || ffn % 64 || batch < 0 || seq < 0 ||
-      (dtype != STAGE_F32 && dtype != STAGE_BF16))
-    return STAGE_EINVAL;
-  // The same allocation calls as stage_init and stage_forward, on stages
-  // that only count bytes: one layer and two layers.
-  int64_t act[2] = {0, 0}, par = 0;
-  for (int L = 1; L <= 2; ++L) {
-    stage_t d;
-    d.dry_run = true;
-    d.L = L;
-    d.h = hidden;
-    d.H = heads;
-    d.f = ffn;
-    d.dtype = dtype;
-    d.esz = dtype == STAGE_BF16 ? 2 : 4;
-    if (L == 1) {
-      for (int w = 0; w < STAGE_NPARAM; ++w) {
-        void* p;
-        const int64_t n = param_numel(&d, w);
-        (void)dev_alloc(&d, d.allocs, &p, n * param_esz(&d, w));
-        (void)dev_alloc(&d, d.allocs, &p, n * 4);
-      }
-      par = d.bytes_param;
-    }
-    if (ensure_activations(&d, batch, seq) != STAGE_OK) return STAGE_EINVAL;
-    act[L - 1] = d.bytes_act;
-  }
-  *per_layer = par + (act[1] - act[0]);
-  *shared = act[0] - (act[1] - act[0]);
+  *per_layer = attn + ffn_b;
+  *shared = sh;
+  return STAGE_OK;
+}
+
+stage_status stage_memory_model_units(int hidden, int heads, int ffn, int batch, int seq,
+                                      stage_dtype dtype, int64_t* attn_unit, int64_t* ffn_unit,
+                                      int64_t* shared) {
+  if (!attn_unit || !ffn_unit || !shared) return STAGE_EINVAL;
+  if (!valid_dims(hidden, heads, ffn, dtype) || batch < 0 || seq < 0) return STAGE_EINVAL;
+  // The same allocation calls as stage_init_units and stage_forward, on
+  // stages that only count bytes: one attention half, one feed-forward
+  // half, and both.  A stage's bytes are the workspace plus the sum over
+  // its units.
+  const int64_t a = dry_bytes(0, 1, hidden, heads, ffn, batch, seq, dtype);
+  const int64_t f = dry_bytes(1, 1, hidden, heads, ffn, batch, seq, dtype);
+  const int64_t af = dry_bytes(0, 2, hidden, heads, ffn, batch, seq, dtype);
+  if (a < 0 || f < 0 || af < 0) return STAGE_EINVAL;
+  *shared = a + f - af;
+  *attn_unit = a - *shared;
+  *ffn_unit = f - *shared;
   return STAGE_OK;
 }
 

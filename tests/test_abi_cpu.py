@@ -78,3 +78,26 @@ def test_mfma_peak_rejects_bad_arguments():
     assert f(None, 0, ctypes.byref(t), ctypes.byref(g)) == 1
     assert f(None, 1 << 25, ctypes.byref(t), ctypes.byref(g)) == 1
     assert f(None, 100, None, ctypes.byref(g)) == 1
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="library not built (run __graft_entry__.build())")
+def test_init_units_rejects_bad_arguments():
+    # unit-range and dims checks come before any device call
+    lib = ctypes.CDLL(LIB)
+    f = lib.stage_init_units
+    f.argtypes = [ctypes.c_int] * 5 + [ctypes.c_uint64, ctypes.c_int, ctypes.c_void_p,
+                                       ctypes.POINTER(ctypes.c_void_p)]
+    f.restype = ctypes.c_int
+    out = ctypes.c_void_p(1)
+    for u0, n, h, H, ffn in [(-1, 2, 128, 2, 256), (0, 0, 128, 2, 256), (3, -1, 128, 2, 256),
+                             ((1 << 30) - 1, 2, 128, 2, 256), (0, 2, 100, 2, 256),
+                             (1, 3, 128, 3, 256), (0, 1, 128, 2, 500)]:
+        assert f(u0, n, h, H, ffn, 0, 1, None, ctypes.byref(out)) == 1, (u0, n, h, H, ffn)
+        assert out.value is None
+    assert f(0, 2, 128, 2, 256, 0, 1, None, None) == 1
+    init = lib.stage_init
+    init.argtypes = [ctypes.c_int] * 4 + [ctypes.c_uint64, ctypes.c_int, ctypes.c_void_p,
+                                          ctypes.POINTER(ctypes.c_void_p)]
+    init.restype = ctypes.c_int
+    assert init(0, 128, 2, 256, 0, 1, None, ctypes.byref(out)) == 1
+    assert init((1 << 29) + 1, 128, 2, 256, 0, 1, None, ctypes.byref(out)) == 1

@@ -7,6 +7,26 @@ import pytest
 import synth
 
 
+def closed_form_units(h, H, f, B, S, bf16):
+    """(attention unit, feed-forward unit) bytes from the storage plan of a
+    half-layer stage: the attention half holds W_qkv, b_qkv, W_o, b_o, g1,
+    be1 (with gradients) and saves X, QKV, the fp32 scores (fp32 stages) or
+    the log-sum-exp, C, x_hat1, rstd1; the feed-forward half holds W_1, b_1,
+    W_2, b_2, g2, be2 and saves its input H1, GELU'(U), G, x_hat2, rstd2."""
+    e = 2 if bf16 else 4
+    T = B * S
+    a = lambda n: max(n, 256)
+    BSS = 0 if bf16 else B * H * S * S
+    attn = (a(3 * h * h * e) + a(3 * h * h * 4) + a(h * h * e) + a(h * h * 4)
+            + sum(a(n * 4) * 2 for n in (3 * h, h, h, h))
+            + a(T * h * e) + a(T * 3 * h * e) + a(BSS * e) + a(B * H * S * 4) + a(T * h * e)
+            + a(T * h * e) + a(T * 4))
+    ffn = (a(f * h * e) + a(f * h * 4) + a(h * f * e) + a(h * f * 4)
+           + sum(a(n * 4) * 2 for n in (f, h, h, h))
+           + a(T * h * e) + a(T * f * e) + a(T * f * e) + a(T * h * e) + a(T * 4))
+    return attn, ffn
+
+
 def closed_form(h, H, f, B, S, bf16):
     """Device bytes of one layer and of the per-stage workspace, from the
     storage plan: parameters in the stage dtype (matrices) or fp32 (vectors)
@@ -43,6 +63,22 @@ def test_memory_model_per_layer_closed_form(cfg):
     # gradients of one layer
     T, h, f = c.batch * c.seq, c.hidden, c.ffn
     assert shared > T * h * 4 + T * f * (2 if bf16 else 4)
+
+
+@pytest.mark.parametrize("cfg", ["tiny", "bert_base_3", "bert_large_4"])
+def test_memory_model_units_closed_form(cfg):
+    import paper_2202_11836_amd as P
+    try:
+        P.load_library()
+    except RuntimeError as e:
+        pytest.skip(str(e))
+    c = synth.CONFIGS[cfg]
+    bf16 = c.dtype == "bf16"
+    code = P.STAGE_BF16 if bf16 else P.STAGE_F32
+    attn, ffn, shared = P.stage_memory_model_units(c.hidden, c.heads, c.ffn, c.batch, c.seq, code)
+    assert (attn, ffn) == closed_form_units(c.hidden, c.heads, c.ffn, c.batch, c.seq, bf16)
+    per_layer, shared_l = P.stage_memory_model(c.hidden, c.heads, c.ffn, c.batch, c.seq, code)
+    assert per_layer == attn + ffn and shared == shared_l
 
 
 def test_memory_model_rejects_bad_dims():
@@ -89,3 +125,22 @@ def test_memory_model_matches_allocations(L, cfg, dtype):
     assert held <= taken + slack and taken <= held + 100 * (2 << 20) + slack
     st.close()
     del y
+
+
+@pytest.mark.gpu
+def test_memory_model_units_matches_allocations():
+    """A stage of units [1, 4) (feed-forward half of layer 0, layer 1) holds
+    shared + attn_unit + 2 ffn_unit bytes."""
+    import torch
+
+    import paper_2202_11836_amd as P
+    c = synth.CONFIGS["bert_base_3"]
+    print("case memory units bert_base_3 [1,4) bf16", flush=True)
+    attn, ffn, shared = P.stage_memory_model_units(c.hidden, c.heads, c.ffn, c.batch, c.seq,
+                                                   P.STAGE_BF16)
+    st = P.Stage(None, c.hidden, c.heads, c.ffn, seed=1, dtype="bf16", first_unit=1, n_units=3)
+    x = torch.zeros(c.batch, c.seq, c.hidden, dtype=torch.bfloat16, device="cuda")
+    st.forward(x)
+    torch.cuda.synchronize()
+    assert st.device_bytes() == shared + attn + 2 * ffn
+    st.close()
