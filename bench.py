@@ -28,12 +28,14 @@ PEAK_HBM_GBS = 8000.0
 # Kernels the roofline entry can report on: a kernel (one compiled
 # instantiation) and the launch sites that use it in one step.
 ROOFLINE_KERNELS = {
-    # weight-gradient GEMM dW = dY^T X over all tokens (split over tokens,
-    # fp32 partials): the kernel with the largest share of step time
-    "wgrad_gemm": ("gemm_bf16_kernel<256, 256, false, false, 4, true>",
-                   ["w2_wgrad_gemm", "w1_wgrad_gemm", "wo_wgrad_gemm", "wqkv_wgrad_gemm"]),
-    "ffn1_gelu_gemm": ("gemm_bf16_kernel<256, 256, true, true, 1, false>", ["ffn1_gelu_gemm_fwd"]),
-    "ffn2_dgrad_dgelu_gemm": ("gemm_bf16_kernel<256, 256, true, true, 2, false>",
+    # the four weight-gradient GEMMs of a layer, dW = dY^T X over all tokens
+    # (split over tokens, fp32 partials), in one group launch: the kernel
+    # with the largest share of step time
+    "wgrad_gemm": ("gemm_bf16_kernel<256, 256, false, false, 4, true, true>",
+                   ["wgrad_group_gemm"]),
+    "ffn1_gelu_gemm": ("gemm_bf16_kernel<256, 256, true, true, 1, false, false>",
+                       ["ffn1_gelu_gemm_fwd"]),
+    "ffn2_dgrad_dgelu_gemm": ("gemm_bf16_kernel<256, 256, true, true, 2, false, false>",
                               ["ffn2_dgrad_dgelu_gemm"]),
 }
 
@@ -55,6 +57,8 @@ def site_flops(site: str, cfg, lengths) -> float:
         "out_dgrad_gemm": 2.0 * T * h * h,
         "wqkv_wgrad_gemm": 2.0 * 3 * h * h * T,
         "qkv_dgrad_resid_gemm": 2.0 * T * h * 3 * h,
+        # W_2, W_1, W_o and W_qkv gradients in one launch
+        "wgrad_group_gemm": 2.0 * T * (2 * h * f + 4 * h * h),
     }
     for k in ("scores_gemm_fwd", "context_gemm_fwd", "dp_gemm_bwd", "dv_gemm_bwd", "dq_gemm_bwd",
               "dk_gemm_bwd"):

@@ -12,6 +12,7 @@
 // transposing LDS read.
 #include <algorithm>
 #include <type_traits>
+#include <vector>
 
 #include "kernels.h"
 
@@ -45,9 +46,9 @@ __device__ __forceinline__ void tile_of_block(int nbm, int nbn, int& tm, int& tn
 // w starts on XCD w % 8 and keeps it (the grid is a multiple of 8), so the
 // tile ranges are dealt out per XCD as above.
 __device__ __forceinline__ void decode_tile(int vt, int total, int nbm, int nbn, int& z, int& tm,
-                                            int& tn) {
+                                            int& tn, bool xcd_remap = true) {
   int bid = vt;
-  if ((total & 7) == 0) bid = (vt & 7) * (total >> 3) + (vt >> 3);
+  if (xcd_remap && (total & 7) == 0) bid = (vt & 7) * (total >> 3) + (vt >> 3);
   const int per_z = nbm * nbn;
   z = bid / per_z;
   const int r0 = bid - z * per_z;
@@ -314,10 +315,11 @@ struct TileOps {
 };
 
 template <int BM, int BN, bool AK, bool BKM>
-__device__ __forceinline__ TileOps tile_ops(const GemmArgs& g, int vt, int total, int nbm, int nbn) {
+__device__ __forceinline__ TileOps tile_ops(const GemmArgs& g, int vt, int total, int nbm, int nbn,
+                                            bool xcd_remap = true) {
   TileOps o;
   int z, tm, tn;
-  decode_tile(vt, total, nbm, nbn, z, tm, tn);
+  decode_tile(vt, total, nbm, nbn, z, tm, tn, xcd_remap);
   o.zs = z % g.ksplit;
   o.zb = z / g.ksplit;
   o.m0 = tm * BM;
@@ -380,26 +382,102 @@ __device__ __forceinline__ void wait_ktile(int after) {
   else wait_vm_lgkm0<0>();
 }
 
+// Group launch: work item j of XCD x (x = work-group index % 8; the grid is
+// a multiple of 8 and dispatch deals work-groups round robin over the XCDs)
+// is item j of the concatenation, over the problems q, of problem q's
+// x-th share [x chunk_q, (x + 1) chunk_q) of its total_q items, so every
+// XCD gets the same share of every problem and its items stay contiguous
+// (L2 reuse).  Returns false past the end of the XCD's list.
+//
+// The group table is read in place from the kernel-argument segment (a
+// by-value argument indexed by a run-time problem number would be copied
+// to scratch memory first).
+typedef const __attribute__((address_space(4))) GemmGroup kgroup_t;
+__device__ __forceinline__ kgroup_t* group_table() {
+  return (kgroup_t*)__builtin_amdgcn_kernarg_segment_ptr();
+}
+
+__device__ __forceinline__ bool group_item(kgroup_t* gg, int j, int& p, int& item) {
+  const int x = blockIdx.x & 7;
+#pragma unroll
+  for (int q = 0; q < GEMM_GROUP_MAX; ++q) {
+    if (q < gg->n) {
+      const int lo = min(gg->total[q], x * gg->chunk[q]);
+      const int hi = min(gg->total[q], lo + gg->chunk[q]);
+      if (j < hi - lo) {
+        p = q;
+        item = lo + j;
+        return true;
+      }
+      j -= hi - lo;
+    }
+  }
+  return false;
+}
+
+__device__ __forceinline__ void group_args(kgroup_t* gg, int p, GemmArgs& g) {
+  const __attribute__((address_space(4))) GemmArgs* a = &gg->g[p];
+  g.A = a->A;
+  g.B = a->B;
+  g.C = a->C;
+  g.C2 = a->C2;
+  g.bias = a->bias;
+  g.aux = a->aux;
+  g.M = a->M;
+  g.N = a->N;
+  g.K = a->K;
+  g.lda = a->lda;
+  g.ldb = a->ldb;
+  g.ldc = a->ldc;
+  g.ldaux = a->ldaux;
+  g.zdiv = a->zdiv;
+  g.sA1 = a->sA1;
+  g.sA2 = a->sA2;
+  g.sB1 = a->sB1;
+  g.sB2 = a->sB2;
+  g.sC1 = a->sC1;
+  g.sC2 = a->sC2;
+  g.ksplit = a->ksplit;
+  g.kchunk = a->kchunk;
+  g.alpha = a->alpha;
+  g.tile = a->tile;
+  g.colpart = a->colpart;
+  g.zdiv_total = a->zdiv_total;
+}
+
 // Persistent kernel: each work-group walks output tiles vt = blockIdx.x,
-// + gridDim.x, ...  The first NS k-tiles of the next output tile are
-// loaded while the current tile's epilogue runs.
-template <int BM, int BN, bool AK, bool BKM, int EPI, bool OUTF32>
-__global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_kernel(GemmArgs g) {
+// + gridDim.x, ... (GROUP: the items of its XCD's list, see group_item).
+// The first NS k-tiles of the next output tile are loaded while the current
+// tile's epilogue runs.
+template <int BM, int BN, bool AK, bool BKM, int EPI, bool OUTF32, bool GROUP = false>
+__global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_kernel(
+    typename std::conditional<GROUP, GemmGroup, GemmArgs>::type ka) {
   using C = TileCfg<BM, BN, AK, BKM>;
   constexpr int TM = C::TM, TN = C::TN, NS = C::NS;
   __shared__ __attribute__((aligned(1024))) char smem[C::LDS_BYTES];
 
-  const int nbm = (g.M + BM - 1) / BM, nbn = (g.N + BN - 1) / BN;
-  const int total = nbm * nbn * g.zdiv_total;
+  GemmArgs g;
+  int nbm, nbn, total, vt, item = 0;
+  if constexpr (GROUP) {
+    vt = blockIdx.x >> 3;
+    int p;
+    if (!group_item(group_table(), vt, p, item)) return;
+    group_args(group_table(), p, g);
+  } else {
+    g = ka;
+    vt = blockIdx.x;
+  }
+  nbm = (g.M + BM - 1) / BM;
+  nbn = (g.N + BN - 1) / BN;
+  total = nbm * nbn * g.zdiv_total;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS DMA targets in SGPRs
   const int wm = wave / C::WGN, wn = wave % C::WGN;
   const int hf = lane >> 5, rr = lane & 31;
   constexpr int KS = C::BK / 16;
 
-  int vt = blockIdx.x;
-  if (vt >= total) return;
-  TileOps T = tile_ops<BM, BN, AK, BKM>(g, vt, total, nbm, nbn);
+  if (!GROUP && vt >= total) return;
+  TileOps T = tile_ops<BM, BN, AK, BKM>(g, GROUP ? item : vt, total, nbm, nbn, !GROUP);
   // First k-tiles of the first output tile.
 #pragma unroll
   for (int t = 0; t < NS; ++t)
@@ -480,7 +558,8 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
     // epilogue (its staging area is separate from the ring).
     __syncthreads();
     const int m0 = T.m0, n0 = T.n0, zs = T.zs, zb = T.zb;
-    const int64_t offC = batch_off(zb, g.zdiv, g.sC1, g.sC2);
+    const GemmArgs ge = g;  // this tile's problem (g moves on to the next tile's)
+    const int64_t offC = batch_off(zb, ge.zdiv, ge.sC1, ge.sC2);
     const int mw = m0 + wm * C::WM, nw = n0 + wn * C::WN;
     constexpr int CH = C::WN / 8;  // 8-column chunks per staged row
     constexpr int QN = 16 * CH / 64;  // chunks per lane per staged 16-row half
@@ -495,16 +574,29 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
         const int c = lane + 64 * q;
         const int row = c / CH, col = (c % CH) * 8;
         const int m = mw + (it >> 1) * 32 + 16 * (it & 1) + row, n = nw + col;
-        dst[q] = (m < g.M && n < g.N)
-                     ? *(const u32x4_t*)((const bf16_t*)g.aux + offC + (int64_t)m * g.ldaux + n)
+        dst[q] = (m < ge.M && n < ge.N)
+                     ? *(const u32x4_t*)((const bf16_t*)ge.aux + offC + (int64_t)m * ge.ldaux + n)
                      : u32x4_t{0, 0, 0, 0};
       }
     };
     if constexpr (AUX) aux_load(0, axv[0]);
-    vt += gridDim.x;
-    const bool more = vt < total;
+    bool more;
+    if constexpr (GROUP) {
+      vt += gridDim.x >> 3;
+      int p;
+      more = group_item(group_table(), vt, p, item);
+      if (more) {
+        group_args(group_table(), p, g);
+        nbm = (g.M + BM - 1) / BM;
+        nbn = (g.N + BN - 1) / BN;
+        total = nbm * nbn * g.zdiv_total;
+      }
+    } else {
+      vt += gridDim.x;
+      more = vt < total;
+    }
     if (more) {
-      T = tile_ops<BM, BN, AK, BKM>(g, vt, total, nbm, nbn);
+      T = tile_ops<BM, BN, AK, BKM>(g, GROUP ? item : vt, total, nbm, nbn, !GROUP);
 #pragma unroll
       for (int t = 0; t < NS; ++t)
         if (t < T.ntiles) issue_ktile<BM, BN, AK, BKM>(g, T, t, smem, wave, lane);
@@ -551,8 +643,8 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
             v[e] = x0[e];
             v[4 + e] = x1[e];
           }
-          if (m < g.M && n < g.N) {
-            epi8<EPI, OUTF32>(g, offC, zs, m, n, v, AUX ? axv[it & 1][q] : u32x4_t{0, 0, 0, 0});
+          if (m < ge.M && n < ge.N) {
+            epi8<EPI, OUTF32>(ge, offC, zs, m, n, v, AUX ? axv[it & 1][q] : u32x4_t{0, 0, 0, 0});
             if (COLSUM) {
 #pragma unroll
               for (int e = 0; e < 8; ++e) csum[e] += v[e];
@@ -562,7 +654,7 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
         __builtin_amdgcn_wave_barrier();
       }
     }
-    if (COLSUM && g.colpart) {
+    if (COLSUM && ge.colpart) {
       // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same columns: fixed-order sum
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -570,8 +662,8 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
         for (int o = CH; o < 64; o <<= 1) csum[e] += __shfl_xor(csum[e], o, 64);
       }
       const int n = nw + (lane % CH) * 8;
-      if (lane < CH && n < g.N) {
-        float* P = g.colpart + (int64_t)(mw / C::WM) * g.N + n;
+      if (lane < CH && n < ge.N) {
+        float* P = ge.colpart + (int64_t)(mw / C::WM) * ge.N + n;
         *(f32x4_t*)P = f32x4_t{csum[0], csum[1], csum[2], csum[3]};
         *(f32x4_t*)(P + 4) = f32x4_t{csum[4], csum[5], csum[6], csum[7]};
       }
@@ -683,6 +775,51 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
     s += b;
     s += c;
     s += d;
+  }
+  for (; z < splits; ++z) s += *(const f32x4_t*)(part + (int64_t)z * mn + i);
+  *(f32x4_t*)(out + i) = s;
+}
+
+struct ReduceGroup {
+  const float* part[GEMM_GROUP_MAX];
+  float* out[GEMM_GROUP_MAX];
+  int64_t mn[GEMM_GROUP_MAX];
+  int splits[GEMM_GROUP_MAX];
+  int blk0[GEMM_GROUP_MAX + 1];  // first block of each problem
+  int n;
+};
+
+// splitk_reduce_kernel over several problems: block b serves the problem q
+// with blk0[q] <= b < blk0[q + 1], in the same per-element order.
+__global__ __launch_bounds__(256) void splitk_reduce_group_kernel(ReduceGroup rg) {
+  const int b = blockIdx.x;
+  int q = 0;
+#pragma unroll
+  for (int k = 1; k < GEMM_GROUP_MAX; ++k)
+    if (k < rg.n && b >= rg.blk0[k]) q = k;
+  const float* part;
+  float* out;
+  int64_t mn;
+  int splits, b0;
+  switch (q) {
+    case 0: part = rg.part[0]; out = rg.out[0]; mn = rg.mn[0]; splits = rg.splits[0]; b0 = rg.blk0[0]; break;
+    case 1: part = rg.part[1]; out = rg.out[1]; mn = rg.mn[1]; splits = rg.splits[1]; b0 = rg.blk0[1]; break;
+    case 2: part = rg.part[2]; out = rg.out[2]; mn = rg.mn[2]; splits = rg.splits[2]; b0 = rg.blk0[2]; break;
+    default: part = rg.part[3]; out = rg.out[3]; mn = rg.mn[3]; splits = rg.splits[3]; b0 = rg.blk0[3]; break;
+  }
+  const int64_t i = ((int64_t)(b - b0) * blockDim.x + threadIdx.x) * 4;
+  if (i >= mn) return;
+  f32x4_t s = *(const f32x4_t*)(part + i);
+  int z = 1;
+  for (; z + 4 <= splits; z += 4) {
+    const f32x4_t a = *(const f32x4_t*)(part + (int64_t)z * mn + i);
+    const f32x4_t c = *(const f32x4_t*)(part + (int64_t)(z + 1) * mn + i);
+    const f32x4_t d = *(const f32x4_t*)(part + (int64_t)(z + 2) * mn + i);
+    const f32x4_t e = *(const f32x4_t*)(part + (int64_t)(z + 3) * mn + i);
+    s += a;
+    s += c;
+    s += d;
+    s += e;
   }
   for (; z < splits; ++z) s += *(const f32x4_t*)(part + (int64_t)z * mn + i);
   *(f32x4_t*)(out + i) = s;
@@ -802,4 +939,112 @@ hipError_t splitk_reduce(const float* part, int splits, int M, int N, float* out
   int blocks = (int)((mn / 4 + 255) / 256);
   hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, st, part, splits, mn, out);
   return hipGetLastError();
+}
+
+hipError_t gemm_bf16_wgrad_group(const GemmArgs* p, int n, hipStream_t st) {
+  if (n < 1 || n > GEMM_GROUP_MAX || !p) return hipErrorInvalidValue;
+  GemmGroup gg{};
+  gg.n = n;
+  int64_t items = 0;
+  for (int q = 0; q < n; ++q) {
+    GemmArgs g = p[q];
+    // the checks gemm_bf16 makes for two m/n-major operands
+    if (g.M < 0 || g.N < 0 || g.K < 0 || g.ksplit < 1) return hipErrorInvalidValue;
+    if (g.N % 8 != 0 || g.ldc % 8 != 0 || g.M % 8 != 0 || g.lda % 8 != 0 || g.ldb % 8 != 0)
+      return hipErrorInvalidValue;
+    if (g.ksplit > 1 && g.kchunk % 64 != 0) return hipErrorInvalidValue;
+    if ((int64_t)g.K * g.lda * 2 >= ((int64_t)1 << 31) ||
+        (int64_t)g.K * g.ldb * 2 >= ((int64_t)1 << 31))
+      return hipErrorInvalidValue;
+    g.zdiv = 1;
+    g.zdiv_total = g.ksplit;
+    g.sA1 = g.sA2 = g.sB1 = g.sB2 = g.sC1 = g.sC2 = 0;
+    gg.g[q] = g;
+    const int64_t t = (int64_t)((g.M + 255) / 256) * ((g.N + 255) / 256) * g.ksplit;
+    if (t >= ((int64_t)1 << 30)) return hipErrorInvalidValue;
+    gg.total[q] = (int)t;
+    gg.chunk[q] = (int)((t + 7) / 8);
+    items += t;
+  }
+  if (items == 0) return hipSuccess;
+  // A multiple of 8 work-groups, one per CU: group_item deals each XCD's
+  // list to the work-groups with that index modulo 8.
+  const int cus = device_cus();
+  const int grid = std::max(8, cus - cus % 8);
+  hipLaunchKernelGGL((gemm_bf16_kernel<256, 256, false, false, EPI_PARTIAL, true, true>),
+                     dim3((unsigned)grid), dim3(TileCfg<256, 256, false, false>::THREADS), 0, st,
+                     gg);
+  return hipGetLastError();
+}
+
+hipError_t splitk_reduce_group(const float* const* part, const int* splits, const int* M,
+                               const int* N, float* const* out, int n, hipStream_t st) {
+  if (n < 1 || n > GEMM_GROUP_MAX) return hipErrorInvalidValue;
+  ReduceGroup rg{};
+  rg.n = n;
+  int64_t blocks = 0;
+  for (int q = 0; q < n; ++q) {
+    const int64_t mn = (int64_t)M[q] * N[q];
+    if (mn < 0 || mn % 4 != 0 || splits[q] < 1) return hipErrorInvalidValue;
+    rg.part[q] = part[q];
+    rg.out[q] = out[q];
+    rg.mn[q] = mn;
+    rg.splits[q] = splits[q];
+    rg.blk0[q] = (int)blocks;
+    blocks += (mn / 4 + 255) / 256;
+    if (blocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+  }
+  rg.blk0[n] = (int)blocks;
+  for (int q = n + 1; q <= GEMM_GROUP_MAX; ++q) rg.blk0[q] = (int)blocks;
+  if (blocks == 0) return hipSuccess;
+  hipLaunchKernelGGL(splitk_reduce_group_kernel, dim3((unsigned)blocks), dim3(256), 0, st, rg);
+  return hipGetLastError();
+}
+
+int wgrad_group_plan(const int* M, const int* N, int n, int K, size_t max_partial, int* chunk_out) {
+  if (n < 1 || n > GEMM_GROUP_MAX || K < 1) return 0;
+  const int cus = device_cus();
+  const int G8 = std::max(8, cus - cus % 8) / 8;  // work-groups per XCD
+  // Cost in k-tile times of one CU: the busiest work-group's k-tiles under
+  // the kernel's deal (group_item: per XCD, problem by problem, split-major;
+  // work-group i of an XCD takes positions i, i + G8, ...), plus the fp32
+  // partials' HBM traffic (written, then read by the reduction: 8 bytes per
+  // element) at about 12 MB per k-tile time (~5 TB/s against a 256 x 256 x
+  // 64 k-tile at ~900 TFLOP/s over the chip).
+  double best = 0.0;
+  int best_ks = 0, best_chunk = 0;
+  std::vector<int> load(G8);
+  for (int ks = 1; ks <= 32; ++ks) {
+    int chunk = (K + ks - 1) / ks;
+    chunk = std::max(64, (chunk + 63) / 64 * 64);
+    const int kse = (K + chunk - 1) / chunk;
+    if (kse != ks) continue;  // same split as a smaller ks
+    size_t partial = 0;
+    for (int q = 0; q < n; ++q) partial += (size_t)kse * M[q] * N[q];
+    if (partial > max_partial) continue;
+    int makespan = 0;
+    for (int x = 0; x < 8; ++x) {
+      std::fill(load.begin(), load.end(), 0);
+      int pos = 0;
+      for (int q = 0; q < n; ++q) {
+        const int tiles = ((M[q] + 255) / 256) * ((N[q] + 255) / 256);
+        const int total = tiles * kse, c = (total + 7) / 8;
+        const int lo = std::min(total, x * c), hi = std::min(total, lo + c);
+        for (int it = lo; it < hi; ++it, ++pos) {
+          const int zs = it / tiles;
+          const int len = std::min(chunk, K - zs * chunk);
+          load[pos % G8] += (len + 63) / 64;
+        }
+      }
+      for (int v : load) makespan = std::max(makespan, v);
+    }
+    const double cost = makespan + (double)partial * 8.0 / 12.0e6;
+    if (best_ks == 0 || cost < best) {
+      best = cost;
+      best_ks = kse;
+      best_chunk = chunk;
+    }
+  }
+  if (best_ks && chunk_out) *chunk_out = best_chunk;
+  return best_ks;
 }

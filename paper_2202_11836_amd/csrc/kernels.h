@@ -63,6 +63,32 @@ hipError_t gemm_f32(const GemmArgs& g, bool a_kmajor, bool b_kmajor, GemmEpi epi
 // out[m][n] = sum_s part[s][m][n] (fixed order), fp32.
 hipError_t splitk_reduce(const float* part, int splits, int M, int N, float* out, hipStream_t st);
 
+// Up to GEMM_GROUP_MAX weight-gradient GEMMs in one launch: each problem
+// p[q] is an EPI_PARTIAL GEMM with both operands m/n-major (A(m, k) =
+// A[k * lda + m], B(k, n) = B[k * ldb + n]: token-major activations and
+// output gradients), batch 1, split over K (ksplit chunks of kchunk, kchunk
+// a multiple of 64), writing fp32 partials to its own C.  Same results as
+// gemm_bf16 on each problem with 256 x 256 tiles.  One persistent
+// work-group per CU serves the problems' tiles from one queue per XCD.
+constexpr int GEMM_GROUP_MAX = 4;
+struct GemmGroup {
+  GemmArgs g[GEMM_GROUP_MAX];
+  int n;
+  int total[GEMM_GROUP_MAX];  // work items (tiles x splits) of problem q
+  int chunk[GEMM_GROUP_MAX];  // per-XCD share of them, ceil(total / 8)
+};
+hipError_t gemm_bf16_wgrad_group(const GemmArgs* p, int n, hipStream_t st);
+// Common split over K for such a group of problems [M[q], N[q]] (host
+// arithmetic): the split count ks (0 if even ks = 1 needs more than
+// max_partial partial elements) and in *chunk its chunk length, chosen for
+// balanced work-groups at little partial traffic, with at most max_partial
+// fp32 partial elements over the group.
+int wgrad_group_plan(const int* M, const int* N, int n, int K, size_t max_partial, int* chunk);
+// splitk_reduce of up to GEMM_GROUP_MAX problems in one launch (same
+// results as one splitk_reduce each).
+hipError_t splitk_reduce_group(const float* const* part, const int* splits, const int* M,
+                               const int* N, float* const* out, int n, hipStream_t st);
+
 // ---------------------------------------------------------------------------
 // Row kernels (one wavefront per row), T = float or bf16_t.
 // ---------------------------------------------------------------------------

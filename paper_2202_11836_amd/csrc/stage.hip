@@ -39,7 +39,8 @@ constexpr int COL_PARTS = 128; // row blocks of the bias-gradient column sums
   X(BQKV_RED, "bqkv_colreduce") X(WQKV_WGRAD, "wqkv_wgrad_gemm")                        \
   X(WQKV_RED, "wqkv_wgrad_splitk_reduce") X(QKV_DGRAD, "qkv_dgrad_resid_gemm")            \
   X(KEXT, "key_extent") X(ATTN_FWD, "attn_fwd") X(ATTN_DQ, "attn_bwd_dq")                 \
-  X(ATTN_DKDV, "attn_bwd_dkdv") X(WT, "weight_transpose")
+  X(ATTN_DKDV, "attn_bwd_dkdv") X(WT, "weight_transpose")                                \
+  X(WGRAD_GROUP, "wgrad_group_gemm") X(WGRAD_GROUP_RED, "wgrad_group_splitk_reduce")
 
 enum Site {
 #define SITE_ENUM(id, name) SITE_##id,
@@ -162,6 +163,7 @@ struct stage {
   void* wt_2 = nullptr;     // [f, h]
   float* splitk = nullptr;  // split-K partials of the weight gradients
   size_t splitk_elems = 0;
+  int wg_T = -1, wg_ks = 0, wg_chunk = 0;  // split of a layer's weight-gradient group for T tokens
 
   int B = 0, S = 0;
   bool have_ctx = false;
@@ -252,6 +254,7 @@ void free_activations(stage_t* s) {
   s->saved.clear();
   s->bytes_act = 0;
   s->cap_T = s->cap_BSS = s->cap_B = s->cap_NQB = -1;
+  s->wg_T = -1;
   s->have_ctx = false;
 }
 
@@ -340,13 +343,24 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
   const int64_t part_elems =
       std::max<int64_t>((int64_t)ln_bwd_blocks((int)T) * 3 * h, (int64_t)COL_PARTS * maxw);
   if ((st = A((void**)&s->part, part_elems * 4))) return st;
-  // Split-K partials: largest weight gradient times its split count.
+  // Split-K partials.  bf16 stages compute a layer's weight gradients in
+  // one group launch: room for all four gradients' partials.  fp32 stages
+  // compute them one at a time: the largest one's.
   size_t need = 0;
   const int64_t shapes[4][2] = {{3 * h, h}, {h, h}, {f, h}, {h, f}};
-  for (auto& mn : shapes) {
-    int tile;
-    int ks = wgrad_split(mn[0], mn[1], (int)T, &tile);
-    if (ks > 1) need = std::max<size_t>(need, (size_t)ks * mn[0] * mn[1]);
+  if (s->dtype == STAGE_BF16) {
+    // the group of a whole layer, as the backward queues it
+    const int Ms[4] = {(int)h, (int)f, (int)h, (int)(3 * h)};
+    const int Ns[4] = {(int)f, (int)h, (int)h, (int)h};
+    int chunk = 0;
+    const int ks = T > 0 ? wgrad_group_plan(Ms, Ns, 4, (int)T, SIZE_MAX, &chunk) : 1;
+    need = (size_t)std::max(ks, 1) * (size_t)(2 * h * f + 4 * h * h);
+  } else {
+    for (auto& mn : shapes) {
+      int tile;
+      int ks = wgrad_split(mn[0], mn[1], (int)T, &tile);
+      if (ks > 1) need = std::max<size_t>(need, (size_t)ks * mn[0] * mn[1]);
+    }
   }
   s->splitk_elems = need;
   if ((st = A((void**)&s->splitk, std::max<size_t>(need, 1) * 4))) return st;
@@ -393,6 +407,64 @@ stage_status wgrad(stage_t* s, int site, int site_red, const T* dYm, int64_t ld_
   } else {
     SITE_I(site, Gemm<T>::run(g, false, false, EPI_STORE, true, 1, s->stream));
   }
+  return STAGE_OK;
+}
+
+// A weight gradient dW[M, N] = dY^T X over the stage's tokens whose launch
+// is deferred to the layer's group launch (bf16 stages).
+struct WgradJob {
+  const void* dy;
+  int64_t ld_dy;
+  const void* x;
+  int64_t ld_x;
+  int M, N;
+  float* out;
+};
+
+// The queued weight gradients of one layer in one GEMM launch (split over
+// tokens, fp32 partials side by side in the split-K buffer) and one
+// fixed-order reduction launch.
+stage_status wgrad_group(stage_t* s, const WgradJob* jobs, int n) {
+  if (n == 0) return STAGE_OK;
+  const int Tn = s->B * s->S;
+  GemmArgs gs[GEMM_GROUP_MAX];
+  float* parts[GEMM_GROUP_MAX];
+  float* outs[GEMM_GROUP_MAX];
+  int spl[GEMM_GROUP_MAX], Ms[GEMM_GROUP_MAX], Ns[GEMM_GROUP_MAX];
+  for (int q = 0; q < n; ++q) {
+    Ms[q] = jobs[q].M;
+    Ns[q] = jobs[q].N;
+  }
+  // One split for the whole group (cached for a whole layer's four).
+  int ks, chunk;
+  if (n == 4 && s->wg_T == Tn) {
+    ks = s->wg_ks;
+    chunk = s->wg_chunk;
+  } else {
+    ks = wgrad_group_plan(Ms, Ns, n, Tn, s->splitk_elems, &chunk);
+    if (ks < 1) return fail(s, STAGE_EHIP, "split-K buffer too small");
+    if (n == 4) {
+      s->wg_T = Tn;
+      s->wg_ks = ks;
+      s->wg_chunk = chunk;
+    }
+  }
+  size_t off = 0;
+  for (int q = 0; q < n; ++q) {
+    const WgradJob& j = jobs[q];
+    parts[q] = s->splitk + off;
+    off += (size_t)ks * j.M * j.N;
+    GemmArgs g = gemm_args(j.dy, j.ld_dy, j.x, j.ld_x, parts[q], j.N, j.M, j.N, Tn);
+    g.ksplit = ks;
+    g.kchunk = chunk;
+    g.tile = 1;
+    gs[q] = g;
+    outs[q] = j.out;
+    spl[q] = ks;
+  }
+  if (off > s->splitk_elems) return fail(s, STAGE_EHIP, "split-K buffer too small");
+  SITE(WGRAD_GROUP, gemm_bf16_wgrad_group(gs, n, s->stream));
+  SITE(WGRAD_GROUP_RED, splitk_reduce_group(parts, spl, Ms, Ns, outs, n, s->stream));
   return STAGE_OK;
 }
 
@@ -560,6 +632,18 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
     const void* W1 = p[STAGE_W_1];
     const void* W2 = p[STAGE_W_2];
     const bool attn = has_attn(s, l), ffn = has_ffn(s, l);
+    // Weight gradients: bf16 stages queue them and compute the layer's in
+    // one group launch at the end of the layer.
+    WgradJob wjobs[GEMM_GROUP_MAX];
+    int nw = 0;
+    auto dW = [&](int site, int site_red, const T* dYm, int64_t ld_dy, const T* Xn,
+                  int64_t ld_x, int M, int N, float* out) -> stage_status {
+      if (kBF) {
+        wjobs[nw++] = {dYm, ld_dy, Xn, ld_x, M, N, out};
+        return STAGE_OK;
+      }
+      return wgrad<T>(s, site, site_red, dYm, ld_dy, Xn, ld_x, M, N, Tn, out);
+    };
     if (kBF) {
       TransposeJob jobs[4];
       int nj = 0;
@@ -586,7 +670,7 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
                               gr[STAGE_G2], gr[STAGE_BE2], gr[STAGE_B_2])))
         return r;
       // dW_2 = dZ2^T G
-      if ((r = wgrad<T>(s, SITE_W2_WGRAD, SITE_W2_RED, dZ2, h, (const T*)v.G, f, h, f, Tn, gr[STAGE_W_2]))) return r;
+      if ((r = dW(SITE_W2_WGRAD, SITE_W2_RED, dZ2, h, (const T*)v.G, f, h, f, gr[STAGE_W_2]))) return r;
       // dU = (dZ2 W_2) * GELU'(U)
       {
         GemmArgs g = gemm_args(dZ2, h, W2, kBF ? h : f, dU, f, Tn, f, h);
@@ -605,7 +689,7 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
         return r;
       }
       // dW_1 = dU^T H1
-      if ((r = wgrad<T>(s, SITE_W1_WGRAD, SITE_W1_RED, dU, f, (const T*)v.H1, h, f, h, Tn, gr[STAGE_W_1]))) return r;
+      if ((r = dW(SITE_W1_WGRAD, SITE_W1_RED, dU, f, (const T*)v.H1, h, f, h, gr[STAGE_W_1]))) return r;
       // dH1 = dZ2 + dU W_1 (the stage's dx when it starts at this layer's
       // feed-forward half)
       T* dH1out = attn ? dH1 : dx;
@@ -617,13 +701,16 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
       }
       dH1in = dH1out;
     }  // feed-forward half
-    if (!attn) break;
+    if (!attn) {
+      if ((r = wgrad_group(s, wjobs, nw))) return r;
+      break;
+    }
     // H1 = LN(Z1): dZ1, dgamma1, dbeta1, db_o
     if ((r = ln_backward<T>(s, SITE_LN1_BWD, SITE_LN1_RED, dH1in, (const T*)v.xhat1, v.rstd1, (const float*)p[STAGE_G1], dZ1,
                             gr[STAGE_G1], gr[STAGE_BE1], gr[STAGE_B_O])))
       return r;
     // dW_o = dZ1^T C
-    if ((r = wgrad<T>(s, SITE_WO_WGRAD, SITE_WO_RED, dZ1, h, (const T*)v.C, h, h, h, Tn, gr[STAGE_W_O]))) return r;
+    if ((r = dW(SITE_WO_WGRAD, SITE_WO_RED, dZ1, h, (const T*)v.C, h, h, h, gr[STAGE_W_O]))) return r;
     // dC = dZ1 W_o
     {
       GemmArgs g = gemm_args(dZ1, h, Wo, h, dC, h, Tn, h, h);
@@ -693,7 +780,7 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
     if (!kBF && (r = col_sum<T>(s, SITE_BQKV_SUM, SITE_BQKV_RED, dQKV, 3 * h, gr[STAGE_B_QKV])))
       return r;
     // dW_qkv = dQKV^T X
-    if ((r = wgrad<T>(s, SITE_WQKV_WGRAD, SITE_WQKV_RED, dQKV, 3 * h, (const T*)v.X, h, 3 * h, h, Tn, gr[STAGE_W_QKV]))) return r;
+    if ((r = dW(SITE_WQKV_WGRAD, SITE_WQKV_RED, dQKV, 3 * h, (const T*)v.X, h, 3 * h, h, gr[STAGE_W_QKV]))) return r;
     // dX = dZ1 + dQKV W_qkv  (the previous layer's dY, or the stage's dx)
     T* dXout = (l > 0) ? (T*)s->dY : dx;
     {
@@ -702,6 +789,7 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
       g.ldaux = h;
       SITE(QKV_DGRAD, Gemm<T>::run(g, true, kBF, EPI_RESID, false, 1, st));
     }
+    if ((r = wgrad_group(s, wjobs, nw))) return r;
     dYcur = dXout;
   }
   return STAGE_OK;
