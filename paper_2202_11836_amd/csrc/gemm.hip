@@ -228,10 +228,11 @@ struct FragPtrs {
 
 
 // Epilogue for 8 consecutive columns n..n+7 of row m (n % 8 == 0, n < N).
-// For EPI_MUL, v returns the values as stored.
+// b0, b1: bias[n .. n + 7] (EPI_STORE with a bias, EPI_GELU), loaded once
+// per tile by the caller.  For EPI_MUL, v returns the values as stored.
 template <int EPI, bool OUTF32>
 __device__ __forceinline__ void epi8(const GemmArgs& g, int64_t offC, int zs, int m, int n,
-                                     float v[8], u32x4_t x) {
+                                     float v[8], u32x4_t x, f32x4_t b0, f32x4_t b1) {
   const int64_t idx = (int64_t)m * g.ldc + n;
   if (EPI == EPI_PARTIAL) {
     float* C = (float*)g.C + (int64_t)zs * g.M * g.ldc + idx;
@@ -245,7 +246,6 @@ __device__ __forceinline__ void epi8(const GemmArgs& g, int64_t offC, int zs, in
       for (int i = 0; i < 8; ++i) v[i] *= g.alpha;
     }
     if (g.bias) {
-      const f32x4_t b0 = *(const f32x4_t*)(g.bias + n), b1 = *(const f32x4_t*)(g.bias + n + 4);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         v[i] += b0[i];
@@ -304,6 +304,28 @@ __device__ __forceinline__ void epi8(const GemmArgs& g, int64_t offC, int zs, in
     }
   }
 
+}
+
+// EPI_MUL / EPI_RESID on 8 values: v * aux or v + aux (aux: 8 packed bf16),
+// rounded to bf16 and packed; v returns the rounded values.
+template <int EPI>
+__device__ __forceinline__ u32x4_t aux8(float v[8], u32x4_t x) {
+  u32x4_t o;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float a0 = __uint_as_float(x[i] << 16), a1 = __uint_as_float(x[i] & 0xffff0000u);
+    if (EPI == EPI_MUL) {
+      v[2 * i] *= a0;
+      v[2 * i + 1] *= a1;
+    } else {
+      v[2 * i] += a0;
+      v[2 * i + 1] += a1;
+    }
+    o[i] = pack_bf16x2(v[2 * i], v[2 * i + 1]);
+    v[2 * i] = __uint_as_float(o[i] << 16);
+    v[2 * i + 1] = __uint_as_float(o[i] & 0xffff0000u);
+  }
+  return o;
 }
 
 // One output tile's operands: buffer resources and k-tile range.
@@ -501,6 +523,21 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
     const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_char_t*)smem;
     pa.init(lds0, wm * C::WM, lane);
     pb.init(lds0 + C::A_BYTES, wn * C::WN, lane);
+    // Bias of the lane's 8 epilogue columns (the same for all its chunks),
+    // loaded once per tile ahead of the wait below: a load in the epilogue
+    // would be waited for behind every store issued before it (loads and
+    // stores share one counter, so the wait has to drain both).
+    constexpr int ECH = C::WN / 8;  // 8-column chunks per staged row
+    static_assert(64 % ECH == 0, "a lane's chunks share their columns");
+    constexpr bool BIAS = EPI == EPI_STORE || EPI == EPI_GELU;
+    f32x4_t bias0 = {0, 0, 0, 0}, bias1 = {0, 0, 0, 0};
+    if (BIAS && g.bias) {
+      const int bn = T.n0 + wn * C::WN + (lane % ECH) * 8;
+      if (bn < g.N) {
+        bias0 = *(const f32x4_t*)(g.bias + bn);
+        bias1 = *(const f32x4_t*)(g.bias + bn + 4);
+      }
+    }
     wait_vm_lgkm0<0>();
     __syncthreads();
     if (ntiles > 0) {
@@ -595,12 +632,22 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
       vt += gridDim.x;
       more = vt < total;
     }
-    if (more) {
-      T = tile_ops<BM, BN, AK, BKM>(g, GROUP ? item : vt, total, nbm, nbn, !GROUP);
+    if (more) T = tile_ops<BM, BN, AK, BKM>(g, GROUP ? item : vt, total, nbm, nbn, !GROUP);
+    auto issue_next = [&]() {
+      if (more) {
 #pragma unroll
-      for (int t = 0; t < NS; ++t)
-        if (t < T.ntiles) issue_ktile<BM, BN, AK, BKM>(g, T, t, smem, wave, lane);
-    }
+        for (int t = 0; t < NS; ++t)
+          if (t < T.ntiles) issue_ktile<BM, BN, AK, BKM>(g, T, t, smem, wave, lane);
+      }
+    };
+    // EPI_MUL / EPI_RESID read an operand per output chunk.  Loads and
+    // stores share one counter, so a load waited for after stores drains
+    // the stores too: these epilogues compute every chunk first (results
+    // packed into the registers the consumed accumulators free), then
+    // request the next tile's k-tiles and store.  The others request the
+    // k-tiles first and store as they go.
+    if constexpr (!AUX) issue_next();
+    u32x4_t res[AUX ? 2 * TM : 1][QN];
 
     // Epilogue.  32x32 accumulator layout: lane holds column (lane % 32);
     // register r holds row 8 * (r / 4) + 4 * (lane / 32) + (r % 4).  Each
@@ -643,16 +690,34 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
             v[e] = x0[e];
             v[4 + e] = x1[e];
           }
-          if (m < ge.M && n < ge.N) {
-            epi8<EPI, OUTF32>(ge, offC, zs, m, n, v, AUX ? axv[it & 1][q] : u32x4_t{0, 0, 0, 0});
-            if (COLSUM) {
+          if constexpr (AUX) {
+            res[it][q] = aux8<EPI>(v, axv[it & 1][q]);
+            // keep the packed result here (not recomputed from fp32 values
+            // held until the stores)
+            asm volatile("" : "+v"(res[it][q]));
+            if (COLSUM && m < ge.M && n < ge.N) {
 #pragma unroll
               for (int e = 0; e < 8; ++e) csum[e] += v[e];
             }
+          } else if (m < ge.M && n < ge.N) {
+            epi8<EPI, OUTF32>(ge, offC, zs, m, n, v, u32x4_t{0, 0, 0, 0}, bias0, bias1);
           }
         }
         __builtin_amdgcn_wave_barrier();
       }
+    }
+    if constexpr (AUX) {
+      issue_next();
+#pragma unroll
+      for (int it = 0; it < 2 * TM; ++it)
+#pragma unroll
+        for (int q = 0; q < QN; ++q) {
+          const int c = lane + 64 * q;
+          const int row = c / CH, col = (c % CH) * 8;
+          const int m = mw + (it >> 1) * 32 + 16 * (it & 1) + row, n = nw + col;
+          if (m < ge.M && n < ge.N)
+            *(u32x4_t*)((bf16_t*)ge.C + offC + (int64_t)m * ge.ldc + n) = res[it][q];
+        }
     }
     if (COLSUM && ge.colpart) {
       // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same columns: fixed-order sum
