@@ -659,51 +659,69 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
     // (CH divides 64) over the rows it writes.
     constexpr bool COLSUM = EPI == EPI_MUL && (CH == 16 || CH == 8) && C::WM == 128;
     float csum[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if constexpr (EPI == EPI_PARTIAL) {
+      // fp32 partials straight from the accumulators (no LDS round trip):
+      // for each register, lanes 0-31 and 32-63 write 32 consecutive
+      // columns of two rows, whole 128-byte lines.
+      float* Cp = (float*)ge.C + (int64_t)zs * ge.M * ge.ldc;
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const int it = 2 * i + half;
-        if constexpr (AUX) {
-          if (it + 1 < 2 * TM) aux_load(it + 1, axv[(it + 1) & 1]);
+        for (int j = 0; j < TN; ++j) {
+          const int n = nw + j * 32 + rr;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int m = mw + i * 32 + 8 * (r >> 2) + 4 * hf + (r & 3);
+            if (m < ge.M && n < ge.N) Cp[(int64_t)m * ge.ldc + n] = acc[i][j][r];
+          }
         }
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-          for (int r = 8 * half; r < 8 * half + 8; ++r) {
-            const int row = 8 * ((r >> 2) & 1) + 4 * hf + (r & 3);  // 0..15
-            const int col = (j * 32 + rr) ^ (hf * 32);
-            stg[row * C::WN + col] = acc[i][j][r];
-          }
-        __builtin_amdgcn_wave_barrier();
-#pragma unroll
-        for (int q = 0; q < QN; ++q) {
-          const int c = lane + 64 * q;
-          const int row = c / CH, col = (c % CH) * 8;
-          const int pcol = col ^ (((row >> 2) & 1) * 32);
-          const int m = mw + i * 32 + 16 * half + row, n = nw + col;
-          float v[8];
-          const f32x4_t x0 = *(const f32x4_t*)(stg + row * C::WN + pcol);
-          const f32x4_t x1 = *(const f32x4_t*)(stg + row * C::WN + pcol + 4);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            v[e] = x0[e];
-            v[4 + e] = x1[e];
-          }
+    } else {
+  #pragma unroll
+      for (int i = 0; i < TM; ++i) {
+  #pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const int it = 2 * i + half;
           if constexpr (AUX) {
-            res[it][q] = aux8<EPI>(v, axv[it & 1][q]);
-            // keep the packed result here (not recomputed from fp32 values
-            // held until the stores)
-            asm volatile("" : "+v"(res[it][q]));
-            if (COLSUM && m < ge.M && n < ge.N) {
-#pragma unroll
-              for (int e = 0; e < 8; ++e) csum[e] += v[e];
-            }
-          } else if (m < ge.M && n < ge.N) {
-            epi8<EPI, OUTF32>(ge, offC, zs, m, n, v, u32x4_t{0, 0, 0, 0}, bias0, bias1);
+            if (it + 1 < 2 * TM) aux_load(it + 1, axv[(it + 1) & 1]);
           }
+  #pragma unroll
+          for (int j = 0; j < TN; ++j)
+  #pragma unroll
+            for (int r = 8 * half; r < 8 * half + 8; ++r) {
+              const int row = 8 * ((r >> 2) & 1) + 4 * hf + (r & 3);  // 0..15
+              const int col = (j * 32 + rr) ^ (hf * 32);
+              stg[row * C::WN + col] = acc[i][j][r];
+            }
+          __builtin_amdgcn_wave_barrier();
+  #pragma unroll
+          for (int q = 0; q < QN; ++q) {
+            const int c = lane + 64 * q;
+            const int row = c / CH, col = (c % CH) * 8;
+            const int pcol = col ^ (((row >> 2) & 1) * 32);
+            const int m = mw + i * 32 + 16 * half + row, n = nw + col;
+            float v[8];
+            const f32x4_t x0 = *(const f32x4_t*)(stg + row * C::WN + pcol);
+            const f32x4_t x1 = *(const f32x4_t*)(stg + row * C::WN + pcol + 4);
+  #pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              v[e] = x0[e];
+              v[4 + e] = x1[e];
+            }
+            if constexpr (AUX) {
+              res[it][q] = aux8<EPI>(v, axv[it & 1][q]);
+              // keep the packed result here (not recomputed from fp32 values
+              // held until the stores)
+              asm volatile("" : "+v"(res[it][q]));
+              if (COLSUM && m < ge.M && n < ge.N) {
+  #pragma unroll
+                for (int e = 0; e < 8; ++e) csum[e] += v[e];
+              }
+            } else if (m < ge.M && n < ge.N) {
+              epi8<EPI, OUTF32>(ge, offC, zs, m, n, v, u32x4_t{0, 0, 0, 0}, bias0, bias1);
+            }
+          }
+          __builtin_amdgcn_wave_barrier();
         }
-        __builtin_amdgcn_wave_barrier();
       }
     }
     if constexpr (AUX) {
