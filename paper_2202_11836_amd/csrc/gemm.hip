@@ -530,12 +530,24 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
     constexpr int ECH = C::WN / 8;  // 8-column chunks per staged row
     static_assert(64 % ECH == 0, "a lane's chunks share their columns");
     constexpr bool BIAS = EPI == EPI_STORE || EPI == EPI_GELU;
+    // fp32 outputs are stored straight from the accumulators (see the
+    // epilogue): the lane's bias is then one value per 32-column block.
+    constexpr bool DIRECT = EPI == EPI_PARTIAL || (EPI == EPI_STORE && OUTF32);
+    static_assert(TN <= 4, "one bias value per 32-column block");
     f32x4_t bias0 = {0, 0, 0, 0}, bias1 = {0, 0, 0, 0};
     if (BIAS && g.bias) {
-      const int bn = T.n0 + wn * C::WN + (lane % ECH) * 8;
-      if (bn < g.N) {
-        bias0 = *(const f32x4_t*)(g.bias + bn);
-        bias1 = *(const f32x4_t*)(g.bias + bn + 4);
+      if constexpr (DIRECT) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int bn = T.n0 + wn * C::WN + 32 * j + (lane & 31);
+          bias0[j] = bn < g.N ? g.bias[bn] : 0.0f;
+        }
+      } else {
+        const int bn = T.n0 + wn * C::WN + (lane % ECH) * 8;
+        if (bn < g.N) {
+          bias0 = *(const f32x4_t*)(g.bias + bn);
+          bias1 = *(const f32x4_t*)(g.bias + bn + 4);
+        }
       }
     }
     wait_vm_lgkm0<0>();
@@ -659,11 +671,12 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
     // (CH divides 64) over the rows it writes.
     constexpr bool COLSUM = EPI == EPI_MUL && (CH == 16 || CH == 8) && C::WM == 128;
     float csum[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    if constexpr (EPI == EPI_PARTIAL) {
-      // fp32 partials straight from the accumulators (no LDS round trip):
-      // for each register, lanes 0-31 and 32-63 write 32 consecutive
-      // columns of two rows, whole 128-byte lines.
-      float* Cp = (float*)ge.C + (int64_t)zs * ge.M * ge.ldc;
+    if constexpr (DIRECT) {
+      // fp32 results (split-K partials, or alpha * acc + bias) straight
+      // from the accumulators, no LDS round trip: for each register, lanes
+      // 0-31 and 32-63 write 32 consecutive columns of two rows, whole
+      // 128-byte lines.
+      float* Cp = (float*)ge.C + (EPI == EPI_PARTIAL ? (int64_t)zs * ge.M * ge.ldc : offC);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -672,7 +685,12 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int m = mw + i * 32 + 8 * (r >> 2) + 4 * hf + (r & 3);
-            if (m < ge.M && n < ge.N) Cp[(int64_t)m * ge.ldc + n] = acc[i][j][r];
+            float v = acc[i][j][r];
+            if (EPI == EPI_STORE) {
+              v *= ge.alpha;
+              if (ge.bias) v += bias0[j];
+            }
+            if (m < ge.M && n < ge.N) Cp[(int64_t)m * ge.ldc + n] = v;
           }
         }
     } else {
