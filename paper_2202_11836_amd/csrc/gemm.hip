@@ -12,7 +12,6 @@
 // transposing LDS read.
 #include <algorithm>
 #include <type_traits>
-#include <vector>
 
 #include "kernels.h"
 
@@ -42,6 +41,10 @@ __device__ __forceinline__ void tile_of_block(int nbm, int nbn, int& tm, int& tn
   tn = r / gsize;
 }
 
+// Tile order inside a z slice: groups of TILE_GM tile-rows, column by column
+// within a group (tiles that share A rows / B columns run close together).
+constexpr int TILE_GM = 8;
+
 // Linear tile index -> (z, m tile, n tile) for a persistent grid.  Work-group
 // w starts on XCD w % 8 and keeps it (the grid is a multiple of 8), so the
 // tile ranges are dealt out per XCD as above.
@@ -52,7 +55,7 @@ __device__ __forceinline__ void decode_tile(int vt, int total, int nbm, int nbn,
   const int per_z = nbm * nbn;
   z = bid / per_z;
   const int r0 = bid - z * per_z;
-  constexpr int GM = 8;
+  constexpr int GM = TILE_GM;
   const int per_group = GM * nbn;
   const int group = r0 / per_group;
   const int first_m = group * GM;
@@ -336,24 +339,22 @@ struct TileOps {
   int m0, n0, zs, zb;
 };
 
+// Operands of output tile (tm, tn) of batch entry zb over k in [kbeg, kend),
+// partial slot zs.
 template <int BM, int BN, bool AK, bool BKM>
-__device__ __forceinline__ TileOps tile_ops(const GemmArgs& g, int vt, int total, int nbm, int nbn,
-                                            bool xcd_remap = true) {
+__device__ __forceinline__ TileOps tile_ops_at(const GemmArgs& g, int zs, int zb, int tm, int tn,
+                                               int kbeg, int kend) {
   TileOps o;
-  int z, tm, tn;
-  decode_tile(vt, total, nbm, nbn, z, tm, tn, xcd_remap);
-  o.zs = z % g.ksplit;
-  o.zb = z / g.ksplit;
+  o.zs = zs;
+  o.zb = zb;
   o.m0 = tm * BM;
   o.n0 = tn * BN;
   const bf16_t* A = (const bf16_t*)g.A + batch_off(o.zb, g.zdiv, g.sA1, g.sA2);
   const bf16_t* B = (const bf16_t*)g.B + batch_off(o.zb, g.zdiv, g.sB1, g.sB2);
-  const int kbeg = o.zs * g.kchunk;
-  const int kend = min(g.K, kbeg + g.kchunk);
   constexpr int BK = TileCfg<BM, BN, AK, BKM>::BK;
   o.ntiles = (kend - kbeg + BK - 1) / BK;
   // k-major: from the tile's first row to the operand's last row (rows past
-  // it read 0; K is a multiple of 64).  m/n-major: from this split's first
+  // it read 0; K is a multiple of 64).  m/n-major: from the range's first
   // k-row and the tile's first column to the end of the operand (k-rows past
   // K read 0; reads past the valid columns of a row only feed output rows /
   // columns that are never stored).
@@ -372,6 +373,15 @@ __device__ __forceinline__ TileOps tile_ops(const GemmArgs& g, int vt, int total
     o.kB0 = 0;
   }
   return o;
+}
+
+template <int BM, int BN, bool AK, bool BKM>
+__device__ __forceinline__ TileOps tile_ops(const GemmArgs& g, int vt, int total, int nbm, int nbn) {
+  int z, tm, tn;
+  decode_tile(vt, total, nbm, nbn, z, tm, tn);
+  const int kbeg = (z % g.ksplit) * g.kchunk;
+  return tile_ops_at<BM, BN, AK, BKM>(g, z % g.ksplit, z / g.ksplit, tm, tn, kbeg,
+                                      min(g.K, kbeg + g.kchunk));
 }
 
 // k-tile t of an output tile -> ring slot t % NS.
@@ -404,37 +414,74 @@ __device__ __forceinline__ void wait_ktile(int after) {
   else wait_vm_lgkm0<0>();
 }
 
-// Group launch: work item j of XCD x (x = work-group index % 8; the grid is
-// a multiple of 8 and dispatch deals work-groups round robin over the XCDs)
-// is item j of the concatenation, over the problems q, of problem q's
-// x-th share [x chunk_q, (x + 1) chunk_q) of its total_q items, so every
-// XCD gets the same share of every problem and its items stay contiguous
-// (L2 reuse).  Returns false past the end of the XCD's list.
-//
+// Group launch (stream-K).  Range r of the G work-groups covers k-tiles
+// [sk_begin(r), sk_begin(r + 1)) of the group's W k-tiles (tiles end to end,
+// each tile's K in k-tiles); work-group w takes range (w % 8) G / 8 + w / 8,
+// so each XCD (work-groups are dealt round robin over the 8 XCDs; the grid
+// is a multiple of 8) works on a contiguous eighth of the tiles.
+__host__ __device__ __forceinline__ int64_t sk_begin(int64_t r, int64_t work, int G) {
+  return r * work / G;
+}
+// The range that holds k-tile x: the largest r with sk_begin(r) <= x (never
+// an empty range).
+__host__ __device__ __forceinline__ int sk_range(int64_t x, int64_t work, int G) {
+  return (int)(((x + 1) * G + work - 1) / work - 1);
+}
+// The two-phase sequence: tile t's first-phase segment (kf k-tiles) starts
+// at t kf, its second-phase segment (kt - kf) at nt kf + t (kt - kf).
+struct SkSeq {
+  int64_t work;
+  int nt, kt, kf, G;
+};
+// Sequence position x -> tile t, k-tile k0 within the tile, k-tiles left in
+// the segment.
+__host__ __device__ __forceinline__ void sk_locate(const SkSeq& q, int64_t x, int& t, int& k0,
+                                                   int& left) {
+  const int64_t p1 = (int64_t)q.nt * q.kf;
+  if (x < p1) {
+    t = (int)(x / q.kf);
+    k0 = (int)(x - (int64_t)t * q.kf);
+    left = q.kf - k0;
+  } else {
+    const int k2 = q.kt - q.kf;
+    const int64_t y = x - p1;
+    t = (int)(y / k2);
+    const int o = (int)(y - (int64_t)t * k2);
+    k0 = q.kf + o;
+    left = k2 - o;
+  }
+}
+// Ranges over tile t's segments: the first phase's [a1, a1 + n1) and the
+// second's [a2, a2 + n2) (n2 = 0 without a second phase); the slot of the
+// piece of range r is r - a1, or n1 + r - a2.
+__host__ __device__ __forceinline__ void sk_tile_ranges(const SkSeq& q, int t, int& a1, int& n1,
+                                                        int& a2, int& n2) {
+  const int64_t s1 = (int64_t)t * q.kf;
+  a1 = sk_range(s1, q.work, q.G);
+  n1 = sk_range(s1 + q.kf - 1, q.work, q.G) - a1 + 1;
+  if (q.kf < q.kt) {
+    const int64_t s2 = (int64_t)q.nt * q.kf + (int64_t)t * (q.kt - q.kf);
+    a2 = sk_range(s2, q.work, q.G);
+    n2 = sk_range(s2 + (q.kt - q.kf) - 1, q.work, q.G) - a2 + 1;
+  } else {
+    a2 = n2 = 0;
+  }
+}
+
+// Position of tile (tm, tn) in a problem's tile order (the inverse of
+// decode_tile for one z slice, without the XCD remap).
+__host__ __device__ __forceinline__ int tile_pos(int tm, int tn, int nbm, int nbn) {
+  const int group = tm / TILE_GM, first_m = group * TILE_GM;
+  const int gsize = min(nbm - first_m, TILE_GM);
+  return group * TILE_GM * nbn + tn * gsize + (tm - first_m);
+}
+
 // The group table is read in place from the kernel-argument segment (a
 // by-value argument indexed by a run-time problem number would be copied
 // to scratch memory first).
 typedef const __attribute__((address_space(4))) GemmGroup kgroup_t;
 __device__ __forceinline__ kgroup_t* group_table() {
   return (kgroup_t*)__builtin_amdgcn_kernarg_segment_ptr();
-}
-
-__device__ __forceinline__ bool group_item(kgroup_t* gg, int j, int& p, int& item) {
-  const int x = blockIdx.x & 7;
-#pragma unroll
-  for (int q = 0; q < GEMM_GROUP_MAX; ++q) {
-    if (q < gg->n) {
-      const int lo = min(gg->total[q], x * gg->chunk[q]);
-      const int hi = min(gg->total[q], lo + gg->chunk[q]);
-      if (j < hi - lo) {
-        p = q;
-        item = lo + j;
-        return true;
-      }
-      j -= hi - lo;
-    }
-  }
-  return false;
 }
 
 __device__ __forceinline__ void group_args(kgroup_t* gg, int p, GemmArgs& g) {
@@ -468,7 +515,7 @@ __device__ __forceinline__ void group_args(kgroup_t* gg, int p, GemmArgs& g) {
 }
 
 // Persistent kernel: each work-group walks output tiles vt = blockIdx.x,
-// + gridDim.x, ... (GROUP: the items of its XCD's list, see group_item).
+// + gridDim.x, ... (GROUP: the pieces of its stream-K range, see sk_begin).
 // The first NS k-tiles of the next output tile are loaded while the current
 // tile's epilogue runs.
 template <int BM, int BN, bool AK, bool BKM, int EPI, bool OUTF32, bool GROUP = false>
@@ -479,27 +526,60 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
   __shared__ __attribute__((aligned(1024))) char smem[C::LDS_BYTES];
 
   GemmArgs g;
-  int nbm, nbn, total, vt, item = 0;
+  int nbm, nbn, total, vt;
+  TileOps T;
+  // GROUP: this work-group's stream-K range [kb, ke) and the length of the
+  // piece being computed.
+  int64_t kb = 0, ke = 0;
+  int plen = 0;
+  const int G = gridDim.x;
+  const int rg = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
+  // The piece of the range that starts at k-tile kb: its problem, tile,
+  // k range and partial slot.
+  auto piece = [&]() {
+    kgroup_t* gt = group_table();
+    const SkSeq sq = {gt->work, gt->tile0[GEMM_GROUP_MAX], gt->kt, gt->kf, G};
+    int t, k0, left;
+    sk_locate(sq, kb, t, k0, left);
+    plen = (int)min<int64_t>(ke - kb, left);
+    int q = 0;
+#pragma unroll
+    for (int qq = 1; qq < GEMM_GROUP_MAX; ++qq)
+      if (qq < gt->n && t >= gt->tile0[qq]) q = qq;
+    group_args(gt, q, g);
+    nbm = (g.M + BM - 1) / BM;
+    nbn = (g.N + BN - 1) / BN;
+    int z, tm, tn;
+    decode_tile(t - gt->tile0[q], nbm * nbn, nbm, nbn, z, tm, tn, false);
+    int a1, n1, a2, n2;
+    sk_tile_ranges(sq, t, a1, n1, a2, n2);
+    const int slot = k0 < gt->kf ? rg - a1 : n1 + rg - a2;
+    T = tile_ops_at<BM, BN, AK, BKM>(g, slot, 0, tm, tn, k0 * C::BK,
+                                     min(g.K, (k0 + plen) * C::BK));
+  };
   if constexpr (GROUP) {
-    vt = blockIdx.x >> 3;
-    int p;
-    if (!group_item(group_table(), vt, p, item)) return;
-    group_args(group_table(), p, g);
+    kgroup_t* gt = group_table();
+    kb = sk_begin(rg, gt->work, G);
+    ke = sk_begin(rg + 1, gt->work, G);
+    if (kb >= ke) return;
+    piece();
+    vt = 0;
+    total = 0;
   } else {
     g = ka;
     vt = blockIdx.x;
+    nbm = (g.M + BM - 1) / BM;
+    nbn = (g.N + BN - 1) / BN;
+    total = nbm * nbn * g.zdiv_total;
+    if (vt >= total) return;
+    T = tile_ops<BM, BN, AK, BKM>(g, vt, total, nbm, nbn);
   }
-  nbm = (g.M + BM - 1) / BM;
-  nbn = (g.N + BN - 1) / BN;
-  total = nbm * nbn * g.zdiv_total;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS DMA targets in SGPRs
   const int wm = wave / C::WGN, wn = wave % C::WGN;
   const int hf = lane >> 5, rr = lane & 31;
   constexpr int KS = C::BK / 16;
 
-  if (!GROUP && vt >= total) return;
-  TileOps T = tile_ops<BM, BN, AK, BKM>(g, GROUP ? item : vt, total, nbm, nbn, !GROUP);
   // First k-tiles of the first output tile.
 #pragma unroll
   for (int t = 0; t < NS; ++t)
@@ -631,20 +711,14 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
     if constexpr (AUX) aux_load(0, axv[0]);
     bool more;
     if constexpr (GROUP) {
-      vt += gridDim.x >> 3;
-      int p;
-      more = group_item(group_table(), vt, p, item);
-      if (more) {
-        group_args(group_table(), p, g);
-        nbm = (g.M + BM - 1) / BM;
-        nbn = (g.N + BN - 1) / BN;
-        total = nbm * nbn * g.zdiv_total;
-      }
+      kb += plen;
+      more = kb < ke;
+      if (more) piece();
     } else {
       vt += gridDim.x;
       more = vt < total;
+      if (more) T = tile_ops<BM, BN, AK, BKM>(g, vt, total, nbm, nbn);
     }
-    if (more) T = tile_ops<BM, BN, AK, BKM>(g, GROUP ? item : vt, total, nbm, nbn, !GROUP);
     auto issue_next = [&]() {
       if (more) {
 #pragma unroll
@@ -881,48 +955,51 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   *(f32x4_t*)(out + i) = s;
 }
 
-struct ReduceGroup {
+// wgrad_group_reduce: block b serves problem q with blk0[q] <= b <
+// blk0[q + 1]; each thread sums 4 consecutive elements of one tile over the
+// tile's pieces (slots) in k order.
+struct SkReduce {
   const float* part[GEMM_GROUP_MAX];
   float* out[GEMM_GROUP_MAX];
-  int64_t mn[GEMM_GROUP_MAX];
-  int splits[GEMM_GROUP_MAX];
-  int blk0[GEMM_GROUP_MAX + 1];  // first block of each problem
+  int M[GEMM_GROUP_MAX], N[GEMM_GROUP_MAX];
+  int blk0[GEMM_GROUP_MAX + 1];
+  int tile0[GEMM_GROUP_MAX];
   int n;
+  SkSeq seq;
 };
 
-// splitk_reduce_kernel over several problems: block b serves the problem q
-// with blk0[q] <= b < blk0[q + 1], in the same per-element order.
-__global__ __launch_bounds__(256) void splitk_reduce_group_kernel(ReduceGroup rg) {
+__global__ __launch_bounds__(256) void wgrad_group_reduce_kernel(SkReduce rd) {
   const int b = blockIdx.x;
   int q = 0;
 #pragma unroll
   for (int k = 1; k < GEMM_GROUP_MAX; ++k)
-    if (k < rg.n && b >= rg.blk0[k]) q = k;
+    if (k < rd.n && b >= rd.blk0[k]) q = k;
   const float* part;
   float* out;
-  int64_t mn;
-  int splits, b0;
+  int M, N, b0, t0;
   switch (q) {
-    case 0: part = rg.part[0]; out = rg.out[0]; mn = rg.mn[0]; splits = rg.splits[0]; b0 = rg.blk0[0]; break;
-    case 1: part = rg.part[1]; out = rg.out[1]; mn = rg.mn[1]; splits = rg.splits[1]; b0 = rg.blk0[1]; break;
-    case 2: part = rg.part[2]; out = rg.out[2]; mn = rg.mn[2]; splits = rg.splits[2]; b0 = rg.blk0[2]; break;
-    default: part = rg.part[3]; out = rg.out[3]; mn = rg.mn[3]; splits = rg.splits[3]; b0 = rg.blk0[3]; break;
+    case 0: part = rd.part[0]; out = rd.out[0]; M = rd.M[0]; N = rd.N[0]; b0 = rd.blk0[0]; t0 = rd.tile0[0]; break;
+    case 1: part = rd.part[1]; out = rd.out[1]; M = rd.M[1]; N = rd.N[1]; b0 = rd.blk0[1]; t0 = rd.tile0[1]; break;
+    case 2: part = rd.part[2]; out = rd.out[2]; M = rd.M[2]; N = rd.N[2]; b0 = rd.blk0[2]; t0 = rd.tile0[2]; break;
+    default: part = rd.part[3]; out = rd.out[3]; M = rd.M[3]; N = rd.N[3]; b0 = rd.blk0[3]; t0 = rd.tile0[3]; break;
   }
+  const int64_t mn = (int64_t)M * N;
   const int64_t i = ((int64_t)(b - b0) * blockDim.x + threadIdx.x) * 4;
   if (i >= mn) return;
+  const int m = (int)(i / N), n = (int)(i - (int64_t)m * N);  // N % 4 == 0: one tile
+  const int nbm = (M + 255) / 256, nbn = (N + 255) / 256;
+  const int t = t0 + tile_pos(m / 256, n / 256, nbm, nbn);
+  const SkSeq sq = rd.seq;
+  int a1, n1, a2, n2;
+  sk_tile_ranges(sq, t, a1, n1, a2, n2);
+  // slot 0 (range a1 holds the tile's first k-tile) is always written; an
+  // empty range wrote no slot
   f32x4_t s = *(const f32x4_t*)(part + i);
-  int z = 1;
-  for (; z + 4 <= splits; z += 4) {
-    const f32x4_t a = *(const f32x4_t*)(part + (int64_t)z * mn + i);
-    const f32x4_t c = *(const f32x4_t*)(part + (int64_t)(z + 1) * mn + i);
-    const f32x4_t d = *(const f32x4_t*)(part + (int64_t)(z + 2) * mn + i);
-    const f32x4_t e = *(const f32x4_t*)(part + (int64_t)(z + 3) * mn + i);
-    s += a;
-    s += c;
-    s += d;
-    s += e;
+  for (int j = 1; j < n1 + n2; ++j) {
+    const int r = j < n1 ? a1 + j : a2 + j - n1;
+    if (sk_begin(r, sq.work, sq.G) < sk_begin(r + 1, sq.work, sq.G))
+      s += *(const f32x4_t*)(part + (int64_t)j * mn + i);
   }
-  for (; z < splits; ++z) s += *(const f32x4_t*)(part + (int64_t)z * mn + i);
   *(f32x4_t*)(out + i) = s;
 }
 
@@ -1042,110 +1119,104 @@ hipError_t splitk_reduce(const float* part, int splits, int M, int N, float* out
   return hipGetLastError();
 }
 
-hipError_t gemm_bf16_wgrad_group(const GemmArgs* p, int n, hipStream_t st) {
-  if (n < 1 || n > GEMM_GROUP_MAX || !p) return hipErrorInvalidValue;
-  GemmGroup gg{};
+namespace {
+
+// Grid of a group launch: one work-group per CU, a multiple of 8.
+int group_grid() {
+  const int cus = device_cus();
+  return std::max(8, cus - cus % 8);
+}
+
+// First-phase k-tiles per tile: the average range, when shorter than a tile.
+int first_phase(int64_t tiles, int kt) {
+  const int64_t w = tiles * kt / group_grid();
+  return (int)std::max<int64_t>(1, std::min<int64_t>(kt, w));
+}
+
+// Checks and the stream-K table of a group; false for invalid problems.
+bool group_table_of(const GemmArgs* p, int n, GemmGroup& gg) {
+  if (n < 1 || n > GEMM_GROUP_MAX || !p) return false;
+  gg = GemmGroup{};
   gg.n = n;
-  int64_t items = 0;
+  int64_t tiles = 0;
   for (int q = 0; q < n; ++q) {
     GemmArgs g = p[q];
-    // the checks gemm_bf16 makes for two m/n-major operands
-    if (g.M < 0 || g.N < 0 || g.K < 0 || g.ksplit < 1) return hipErrorInvalidValue;
+    // the checks gemm_bf16 makes for two m/n-major operands; one K for all
+    if (g.M < 0 || g.N < 0 || g.K < 1 || g.K != p[0].K) return false;
     if (g.N % 8 != 0 || g.ldc % 8 != 0 || g.M % 8 != 0 || g.lda % 8 != 0 || g.ldb % 8 != 0)
-      return hipErrorInvalidValue;
-    if (g.ksplit > 1 && g.kchunk % 64 != 0) return hipErrorInvalidValue;
+      return false;
     if ((int64_t)g.K * g.lda * 2 >= ((int64_t)1 << 31) ||
         (int64_t)g.K * g.ldb * 2 >= ((int64_t)1 << 31))
-      return hipErrorInvalidValue;
+      return false;
     g.zdiv = 1;
-    g.zdiv_total = g.ksplit;
+    g.ksplit = 1;
+    g.kchunk = g.K;
+    g.zdiv_total = 1;
     g.sA1 = g.sA2 = g.sB1 = g.sB2 = g.sC1 = g.sC2 = 0;
     gg.g[q] = g;
-    const int64_t t = (int64_t)((g.M + 255) / 256) * ((g.N + 255) / 256) * g.ksplit;
-    if (t >= ((int64_t)1 << 30)) return hipErrorInvalidValue;
-    gg.total[q] = (int)t;
-    gg.chunk[q] = (int)((t + 7) / 8);
-    items += t;
+    gg.tile0[q] = (int)tiles;
+    tiles += (int64_t)((g.M + 255) / 256) * ((g.N + 255) / 256);
+    if (tiles >= ((int64_t)1 << 24)) return false;
   }
-  if (items == 0) return hipSuccess;
-  // A multiple of 8 work-groups, one per CU: group_item deals each XCD's
-  // list to the work-groups with that index modulo 8.
-  const int cus = device_cus();
-  const int grid = std::max(8, cus - cus % 8);
+  gg.tile0[n] = (int)tiles;
+  for (int q = n + 1; q <= GEMM_GROUP_MAX; ++q) gg.tile0[q] = (int)tiles;
+  gg.kt = (p[0].K + 63) / 64;
+  gg.work = tiles * gg.kt;
+  gg.kf = first_phase(tiles, gg.kt);
+  return true;
+}
+
+}  // namespace
+
+int wgrad_group_slots(const int* M, const int* N, int n, int K) {
+  if (n < 1 || n > GEMM_GROUP_MAX || K < 1) return 0;
+  int64_t tiles = 0;
+  for (int q = 0; q < n; ++q) {
+    if (M[q] < 0 || N[q] < 0) return 0;
+    tiles += (int64_t)((M[q] + 255) / 256) * ((N[q] + 255) / 256);
+  }
+  if (tiles == 0) return 1;
+  const int kt = (K + 63) / 64;
+  const SkSeq sq = {tiles * kt, (int)tiles, kt, first_phase(tiles, kt), group_grid()};
+  int slots = 1;
+  for (int t = 0; t < (int)tiles; ++t) {
+    int a1, n1, a2, n2;
+    sk_tile_ranges(sq, t, a1, n1, a2, n2);
+    slots = std::max(slots, n1 + n2);
+  }
+  return slots;
+}
+
+hipError_t gemm_bf16_wgrad_group(const GemmArgs* p, int n, hipStream_t st) {
+  GemmGroup gg;
+  if (!group_table_of(p, n, gg)) return hipErrorInvalidValue;
+  if (gg.work == 0) return hipSuccess;
   hipLaunchKernelGGL((gemm_bf16_kernel<256, 256, false, false, EPI_PARTIAL, true, true>),
-                     dim3((unsigned)grid), dim3(TileCfg<256, 256, false, false>::THREADS), 0, st,
-                     gg);
+                     dim3((unsigned)group_grid()), dim3(TileCfg<256, 256, false, false>::THREADS),
+                     0, st, gg);
   return hipGetLastError();
 }
 
-hipError_t splitk_reduce_group(const float* const* part, const int* splits, const int* M,
-                               const int* N, float* const* out, int n, hipStream_t st) {
-  if (n < 1 || n > GEMM_GROUP_MAX) return hipErrorInvalidValue;
-  ReduceGroup rg{};
-  rg.n = n;
+hipError_t wgrad_group_reduce(const GemmArgs* p, float* const* out, int n, hipStream_t st) {
+  GemmGroup gg;
+  if (!group_table_of(p, n, gg) || !out) return hipErrorInvalidValue;
+  SkReduce rd{};
+  rd.n = n;
+  rd.seq = {gg.work, gg.tile0[n], gg.kt, gg.kf, group_grid()};
   int64_t blocks = 0;
   for (int q = 0; q < n; ++q) {
-    const int64_t mn = (int64_t)M[q] * N[q];
-    if (mn < 0 || mn % 4 != 0 || splits[q] < 1) return hipErrorInvalidValue;
-    rg.part[q] = part[q];
-    rg.out[q] = out[q];
-    rg.mn[q] = mn;
-    rg.splits[q] = splits[q];
-    rg.blk0[q] = (int)blocks;
-    blocks += (mn / 4 + 255) / 256;
+    if (p[q].ldc != p[q].N) return hipErrorInvalidValue;  // partial slots are dense M x N
+    rd.part[q] = (const float*)p[q].C;
+    rd.out[q] = out[q];
+    rd.M[q] = p[q].M;
+    rd.N[q] = p[q].N;
+    rd.tile0[q] = gg.tile0[q];
+    rd.blk0[q] = (int)blocks;
+    blocks += ((int64_t)p[q].M * p[q].N / 4 + 255) / 256;
     if (blocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
   }
-  rg.blk0[n] = (int)blocks;
-  for (int q = n + 1; q <= GEMM_GROUP_MAX; ++q) rg.blk0[q] = (int)blocks;
+  for (int q = n; q <= GEMM_GROUP_MAX; ++q) rd.blk0[q] = (int)blocks;
   if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL(splitk_reduce_group_kernel, dim3((unsigned)blocks), dim3(256), 0, st, rg);
+  hipLaunchKernelGGL(wgrad_group_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, st, rd);
   return hipGetLastError();
-}
-
-int wgrad_group_plan(const int* M, const int* N, int n, int K, size_t max_partial, int* chunk_out) {
-  if (n < 1 || n > GEMM_GROUP_MAX || K < 1) return 0;
-  const int cus = device_cus();
-  const int G8 = std::max(8, cus - cus % 8) / 8;  // work-groups per XCD
-  // Cost in k-tile times of one CU: the busiest work-group's k-tiles under
-  // the kernel's deal (group_item: per XCD, problem by problem, split-major;
-  // work-group i of an XCD takes positions i, i + G8, ...), plus the fp32
-  // partials' HBM traffic (written, then read by the reduction: 8 bytes per
-  // element) at about 12 MB per k-tile time (~5 TB/s against a 256 x 256 x
-  // 64 k-tile at ~900 TFLOP/s over the chip).
-  double best = 0.0;
-  int best_ks = 0, best_chunk = 0;
-  std::vector<int> load(G8);
-  for (int ks = 1; ks <= 32; ++ks) {
-    int chunk = (K + ks - 1) / ks;
-    chunk = std::max(64, (chunk + 63) / 64 * 64);
-    const int kse = (K + chunk - 1) / chunk;
-    if (kse != ks) continue;  // same split as a smaller ks
-    size_t partial = 0;
-    for (int q = 0; q < n; ++q) partial += (size_t)kse * M[q] * N[q];
-    if (partial > max_partial) continue;
-    int makespan = 0;
-    for (int x = 0; x < 8; ++x) {
-      std::fill(load.begin(), load.end(), 0);
-      int pos = 0;
-      for (int q = 0; q < n; ++q) {
-        const int tiles = ((M[q] + 255) / 256) * ((N[q] + 255) / 256);
-        const int total = tiles * kse, c = (total + 7) / 8;
-        const int lo = std::min(total, x * c), hi = std::min(total, lo + c);
-        for (int it = lo; it < hi; ++it, ++pos) {
-          const int zs = it / tiles;
-          const int len = std::min(chunk, K - zs * chunk);
-          load[pos % G8] += (len + 63) / 64;
-        }
-      }
-      for (int v : load) makespan = std::max(makespan, v);
-    }
-    const double cost = makespan + (double)partial * 8.0 / 12.0e6;
-    if (best_ks == 0 || cost < best) {
-      best = cost;
-      best_ks = kse;
-      best_chunk = chunk;
-    }
-  }
-  if (best_ks && chunk_out) *chunk_out = best_chunk;
-  return best_ks;
 }

@@ -63,31 +63,36 @@ hipError_t gemm_f32(const GemmArgs& g, bool a_kmajor, bool b_kmajor, GemmEpi epi
 // out[m][n] = sum_s part[s][m][n] (fixed order), fp32.
 hipError_t splitk_reduce(const float* part, int splits, int M, int N, float* out, hipStream_t st);
 
-// Up to GEMM_GROUP_MAX weight-gradient GEMMs in one launch: each problem
-// p[q] is an EPI_PARTIAL GEMM with both operands m/n-major (A(m, k) =
-// A[k * lda + m], B(k, n) = B[k * ldb + n]: token-major activations and
-// output gradients), batch 1, split over K (ksplit chunks of kchunk, kchunk
-// a multiple of 64), writing fp32 partials to its own C.  Same results as
-// gemm_bf16 on each problem with 256 x 256 tiles.  One persistent
-// work-group per CU serves the problems' tiles from one queue per XCD.
+// Up to GEMM_GROUP_MAX weight-gradient GEMMs in one launch, stream-K: each
+// problem p[q] is a GEMM with both operands m/n-major (A(m, k) = A[k * lda +
+// m], B(k, n) = B[k * ldb + n]: token-major activations and output
+// gradients), batch 1, and all share one K.  The k-tiles (of 64) of their
+// 256 x 256 tiles are laid end to end in two phases, the first kf k-tiles
+// of every tile, then the rest of every tile, and the sequence is cut into
+// one contiguous range per work-group (one work-group per CU); kf is the
+// average range length when a tile holds more than that, so that the
+// work-groups of the first phase each own one tile's first kf k-tiles and
+// all run over the same k at the same time.  The part of a range inside one
+// tile's phase (a piece) writes an fp32 partial to slot j of its problem's C
+// (C + j * M * ldc), j = its rank among that tile's pieces in k order;
+// wgrad_group_reduce then sums each tile's pieces in k order.  ksplit /
+// kchunk of p[q] are ignored.
 constexpr int GEMM_GROUP_MAX = 4;
 struct GemmGroup {
   GemmArgs g[GEMM_GROUP_MAX];
   int n;
-  int total[GEMM_GROUP_MAX];  // work items (tiles x splits) of problem q
-  int chunk[GEMM_GROUP_MAX];  // per-XCD share of them, ceil(total / 8)
+  int tile0[GEMM_GROUP_MAX + 1];  // first (global) tile of each problem; tile0[n] = all tiles
+  int kt;                         // k-tiles per tile, ceil(K / 64)
+  int kf;                         // k-tiles of each tile in the first phase
+  int64_t work;                   // k-tiles over all tiles, tile0[n] * kt
 };
+// Slots of M x N fp32 partials each problem's C must hold for such a group
+// (the most pieces of one tile) on this device; 0 for invalid sizes.
+int wgrad_group_slots(const int* M, const int* N, int n, int K);
 hipError_t gemm_bf16_wgrad_group(const GemmArgs* p, int n, hipStream_t st);
-// Common split over K for such a group of problems [M[q], N[q]] (host
-// arithmetic): the split count ks (0 if even ks = 1 needs more than
-// max_partial partial elements) and in *chunk its chunk length, chosen for
-// balanced work-groups at little partial traffic, with at most max_partial
-// fp32 partial elements over the group.
-int wgrad_group_plan(const int* M, const int* N, int n, int K, size_t max_partial, int* chunk);
-// splitk_reduce of up to GEMM_GROUP_MAX problems in one launch (same
-// results as one splitk_reduce each).
-hipError_t splitk_reduce_group(const float* const* part, const int* splits, const int* M,
-                               const int* N, float* const* out, int n, hipStream_t st);
+// out[q][m][n] = the sum over the pieces of (m, n)'s tile of slot j of
+// p[q].C, in k order (same p as the GEMM launch).
+hipError_t wgrad_group_reduce(const GemmArgs* p, float* const* out, int n, hipStream_t st);
 
 // ---------------------------------------------------------------------------
 // Row kernels (one wavefront per row), T = float or bf16_t.

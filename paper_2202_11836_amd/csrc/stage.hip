@@ -163,7 +163,6 @@ struct stage {
   void* wt_2 = nullptr;     // [f, h]
   float* splitk = nullptr;  // split-K partials of the weight gradients
   size_t splitk_elems = 0;
-  int wg_T = -1, wg_ks = 0, wg_chunk = 0;  // split of a layer's weight-gradient group for T tokens
 
   int B = 0, S = 0;
   bool have_ctx = false;
@@ -254,7 +253,6 @@ void free_activations(stage_t* s) {
   s->saved.clear();
   s->bytes_act = 0;
   s->cap_T = s->cap_BSS = s->cap_B = s->cap_NQB = -1;
-  s->wg_T = -1;
   s->have_ctx = false;
 }
 
@@ -349,12 +347,14 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
   size_t need = 0;
   const int64_t shapes[4][2] = {{3 * h, h}, {h, h}, {f, h}, {h, f}};
   if (s->dtype == STAGE_BF16) {
-    // the group of a whole layer, as the backward queues it
+    // the groups the backward launches: a whole layer (W_2, W_1, W_o,
+    // W_qkv), or the feed-forward or attention half of a partial layer
     const int Ms[4] = {(int)h, (int)f, (int)h, (int)(3 * h)};
     const int Ns[4] = {(int)f, (int)h, (int)h, (int)h};
-    int chunk = 0;
-    const int ks = T > 0 ? wgrad_group_plan(Ms, Ns, 4, (int)T, SIZE_MAX, &chunk) : 1;
-    need = (size_t)std::max(ks, 1) * (size_t)(2 * h * f + 4 * h * h);
+    const int K = (int)std::max<int64_t>(T, 1);
+    need = std::max({(size_t)wgrad_group_slots(Ms, Ns, 4, K) * (size_t)(2 * h * f + 4 * h * h),
+                     (size_t)wgrad_group_slots(Ms, Ns, 2, K) * (size_t)(2 * h * f),
+                     (size_t)wgrad_group_slots(Ms + 2, Ns + 2, 2, K) * (size_t)(4 * h * h)});
   } else {
     for (auto& mn : shapes) {
       int tile;
@@ -421,50 +421,32 @@ struct WgradJob {
   float* out;
 };
 
-// The queued weight gradients of one layer in one GEMM launch (split over
-// tokens, fp32 partials side by side in the split-K buffer) and one
-// fixed-order reduction launch.
+// The queued weight gradients of one layer in one GEMM launch (stream-K
+// over all their tiles, fp32 partials side by side in the split-K buffer)
+// and one fixed-order reduction launch.
 stage_status wgrad_group(stage_t* s, const WgradJob* jobs, int n) {
   if (n == 0) return STAGE_OK;
   const int Tn = s->B * s->S;
   GemmArgs gs[GEMM_GROUP_MAX];
-  float* parts[GEMM_GROUP_MAX];
   float* outs[GEMM_GROUP_MAX];
-  int spl[GEMM_GROUP_MAX], Ms[GEMM_GROUP_MAX], Ns[GEMM_GROUP_MAX];
+  int Ms[GEMM_GROUP_MAX], Ns[GEMM_GROUP_MAX];
   for (int q = 0; q < n; ++q) {
     Ms[q] = jobs[q].M;
     Ns[q] = jobs[q].N;
   }
-  // One split for the whole group (cached for a whole layer's four).
-  int ks, chunk;
-  if (n == 4 && s->wg_T == Tn) {
-    ks = s->wg_ks;
-    chunk = s->wg_chunk;
-  } else {
-    ks = wgrad_group_plan(Ms, Ns, n, Tn, s->splitk_elems, &chunk);
-    if (ks < 1) return fail(s, STAGE_EHIP, "split-K buffer too small");
-    if (n == 4) {
-      s->wg_T = Tn;
-      s->wg_ks = ks;
-      s->wg_chunk = chunk;
-    }
-  }
+  const int slots = wgrad_group_slots(Ms, Ns, n, Tn);
+  if (slots < 1) return fail(s, STAGE_EINVAL, "weight-gradient group: invalid sizes");
   size_t off = 0;
   for (int q = 0; q < n; ++q) {
     const WgradJob& j = jobs[q];
-    parts[q] = s->splitk + off;
-    off += (size_t)ks * j.M * j.N;
-    GemmArgs g = gemm_args(j.dy, j.ld_dy, j.x, j.ld_x, parts[q], j.N, j.M, j.N, Tn);
-    g.ksplit = ks;
-    g.kchunk = chunk;
-    g.tile = 1;
-    gs[q] = g;
+    gs[q] = gemm_args(j.dy, j.ld_dy, j.x, j.ld_x, s->splitk + off, j.N, j.M, j.N, Tn);
+    gs[q].tile = 1;
+    off += (size_t)slots * j.M * j.N;
     outs[q] = j.out;
-    spl[q] = ks;
   }
   if (off > s->splitk_elems) return fail(s, STAGE_EHIP, "split-K buffer too small");
   SITE(WGRAD_GROUP, gemm_bf16_wgrad_group(gs, n, s->stream));
-  SITE(WGRAD_GROUP_RED, splitk_reduce_group(parts, spl, Ms, Ns, outs, n, s->stream));
+  SITE(WGRAD_GROUP_RED, wgrad_group_reduce(gs, outs, n, s->stream));
   return STAGE_OK;
 }
 
