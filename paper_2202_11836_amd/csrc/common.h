@@ -77,3 +77,26 @@ __device__ __forceinline__ float gelu_grad_f(float u) {
   const GeluParts p = gelu_parts(u);
   return fmaf(u * 0.39894228040143268f, p.e, p.cdf);
 }
+
+// One block (256 threads) of a column reduction: out[c .. c + 15] (16
+// columns from bx * 16) = the sum over partial rows b < nblk of
+// part[(b * nvec + v) * n + c]; 4 threads x 4 columns per partial row, 64
+// stripes of rows, the stripe sums combined in LDS (sm) by a fixed-order
+// tree.  out may be null (nothing stored).
+__device__ __forceinline__ void colred_block(const float* __restrict__ part, int nblk, int nvec,
+                                             int n, int v, int bx, float* out, f32x4_t (*sm)[4]) {
+  const int q = threadIdx.x & 3, stripe = threadIdx.x >> 2;
+  const int c = bx * 16 + 4 * q;
+  f32x4_t s = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (c < n) {
+#pragma unroll 8
+    for (int b = stripe; b < nblk; b += 64) s += *(const f32x4_t*)(part + ((int64_t)b * nvec + v) * n + c);
+  }
+  sm[stripe][q] = s;
+  __syncthreads();
+  for (int w = 32; w > 0; w >>= 1) {
+    if (stripe < w) sm[stripe][q] += sm[stripe + w][q];
+    __syncthreads();
+  }
+  if (stripe == 0 && c < n && out) *(f32x4_t*)(out + c) = sm[0][q];
+}

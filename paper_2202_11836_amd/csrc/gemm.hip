@@ -966,10 +966,40 @@ struct SkReduce {
   int tile0[GEMM_GROUP_MAX];
   int n;
   SkSeq seq;
+  // column reductions: job j owns blocks [cblk0[j], cblk0[j + 1]) after the
+  // split-K blocks, ceil(n / 16) per output vector
+  ColJob col[COLJOB_MAX];
+  int cblk0[COLJOB_MAX + 1];
+  int ncol;
 };
 
 __global__ __launch_bounds__(256) void wgrad_group_reduce_kernel(SkReduce rd) {
   const int b = blockIdx.x;
+  if (b >= rd.blk0[rd.n]) {  // a column-reduction block (block-uniform branch)
+    __shared__ f32x4_t sm[64][4];
+    int j = 0;
+#pragma unroll
+    for (int k = 1; k < COLJOB_MAX; ++k)
+      if (k < rd.ncol && b >= rd.cblk0[k]) j = k;
+    ColJob cj;
+    switch (j) {
+      case 0: cj = rd.col[0]; break;
+      case 1: cj = rd.col[1]; break;
+      case 2: cj = rd.col[2]; break;
+      default: cj = rd.col[3]; break;
+    }
+    const int nx = (cj.n + 15) / 16, lb = b - rd.cblk0[j];
+    const int v = lb / nx;
+    float* o;
+    switch (v) {
+      case 0: o = cj.out[0]; break;
+      case 1: o = cj.out[1]; break;
+      case 2: o = cj.out[2]; break;
+      default: o = cj.out[3]; break;
+    }
+    colred_block(cj.part, cj.nblk, cj.nvec, cj.n, v, lb - v * nx, o, sm);
+    return;
+  }
   int q = 0;
 #pragma unroll
   for (int k = 1; k < GEMM_GROUP_MAX; ++k)
@@ -1197,9 +1227,11 @@ hipError_t gemm_bf16_wgrad_group(const GemmArgs* p, int n, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t wgrad_group_reduce(const GemmArgs* p, float* const* out, int n, hipStream_t st) {
+hipError_t wgrad_group_reduce(const GemmArgs* p, float* const* out, int n, const ColJob* cols,
+                              int ncols, hipStream_t st) {
   GemmGroup gg;
-  if (!group_table_of(p, n, gg) || !out) return hipErrorInvalidValue;
+  if (!group_table_of(p, n, gg) || !out || ncols < 0 || ncols > COLJOB_MAX || (ncols && !cols))
+    return hipErrorInvalidValue;
   SkReduce rd{};
   rd.n = n;
   rd.seq = {gg.work, gg.tile0[n], gg.kt, gg.kf, group_grid()};
@@ -1216,6 +1248,17 @@ hipError_t wgrad_group_reduce(const GemmArgs* p, float* const* out, int n, hipSt
     if (blocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
   }
   for (int q = n; q <= GEMM_GROUP_MAX; ++q) rd.blk0[q] = (int)blocks;
+  rd.ncol = ncols;
+  for (int j = 0; j < ncols; ++j) {
+    const ColJob& c = cols[j];
+    if (c.nvec < 1 || c.nvec > 4 || c.n < 0 || c.n % 4 != 0 || c.nblk < 0 || !c.part)
+      return hipErrorInvalidValue;
+    rd.col[j] = c;
+    rd.cblk0[j] = (int)blocks;
+    blocks += (int64_t)((c.n + 15) / 16) * c.nvec;
+    if (blocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+  }
+  for (int j = ncols; j <= COLJOB_MAX; ++j) rd.cblk0[j] = (int)blocks;
   if (blocks == 0) return hipSuccess;
   hipLaunchKernelGGL(wgrad_group_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, st, rd);
   return hipGetLastError();

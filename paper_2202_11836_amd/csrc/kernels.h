@@ -90,9 +90,20 @@ struct GemmGroup {
 // (the most pieces of one tile) on this device; 0 for invalid sizes.
 int wgrad_group_slots(const int* M, const int* N, int n, int K);
 hipError_t gemm_bf16_wgrad_group(const GemmArgs* p, int n, hipStream_t st);
+// A column reduction run with a group's reduction: out[v][c] = the sum over
+// the nblk partial rows b of part[(b * nvec + v) * n + c], v < nvec <= 4, in
+// col_reduce's order (null outputs are skipped).
+struct ColJob {
+  const float* part;
+  int nblk, nvec, n;
+  float* out[4];
+};
+constexpr int COLJOB_MAX = 4;
 // out[q][m][n] = the sum over the pieces of (m, n)'s tile of slot j of
-// p[q].C, in k order (same p as the GEMM launch).
-hipError_t wgrad_group_reduce(const GemmArgs* p, float* const* out, int n, hipStream_t st);
+// p[q].C, in k order (same p as the GEMM launch), and the ncols <=
+// COLJOB_MAX column reductions cols, in one launch.
+hipError_t wgrad_group_reduce(const GemmArgs* p, float* const* out, int n, const ColJob* cols,
+                              int ncols, hipStream_t st);
 
 // ---------------------------------------------------------------------------
 // Row kernels (one wavefront per row), T = float or bf16_t.

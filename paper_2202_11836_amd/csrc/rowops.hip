@@ -368,26 +368,11 @@ struct OutPtrs {
   float* p[4];
 };
 
-// 16 columns per block: 4 threads x 4 columns per partial row, 64 stripes of
-// partial rows; the stripe sums are combined in LDS by a fixed-order tree.
+// 16 columns per block (colred_block), grid (ceil(n / 16), nvec).
 __global__ __launch_bounds__(256) void col_reduce_kernel(const float* __restrict__ part, int nblk,
                                                          int nvec, int n, OutPtrs outs) {
   __shared__ f32x4_t sm[64][4];
-  const int q = threadIdx.x & 3, stripe = threadIdx.x >> 2;
-  const int c = blockIdx.x * 16 + 4 * q;
-  const int v = blockIdx.y;
-  f32x4_t s = {0.0f, 0.0f, 0.0f, 0.0f};
-  if (c < n) {
-#pragma unroll 8
-    for (int b = stripe; b < nblk; b += 64) s += *(const f32x4_t*)(part + ((int64_t)b * nvec + v) * n + c);
-  }
-  sm[stripe][q] = s;
-  __syncthreads();
-  for (int w = 32; w > 0; w >>= 1) {
-    if (stripe < w) sm[stripe][q] += sm[stripe + w][q];
-    __syncthreads();
-  }
-  if (stripe == 0 && c < n && outs.p[v]) *(f32x4_t*)(outs.p[v] + c) = sm[0][q];
+  colred_block(part, nblk, nvec, n, blockIdx.y, blockIdx.x, outs.p[blockIdx.y], sm);
 }
 
 // P = softmax over keys of scale * scores, masked keys -> 0, empty rows -> 0.

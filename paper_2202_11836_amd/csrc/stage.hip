@@ -153,6 +153,7 @@ struct stage {
   void* dC = nullptr;       // [T, h]
   void* dY = nullptr;       // [T, h] gradient flowing between layers
   float* part = nullptr;    // column-sum partials
+  float* part2 = nullptr;   // second LayerNorm's partials (bf16: reduced at the layer's end)
   float* colpart_ffn = nullptr;  // [ceil(T/128), f] column sums of dU (bf16 stages)
   float* colpart_qkv = nullptr;  // [B * ceil(S/32), 3h] column sums of dQKV (bf16 stages)
   // Transposed weights of the layer being differentiated (bf16 stages), so
@@ -341,6 +342,9 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
   const int64_t part_elems =
       std::max<int64_t>((int64_t)ln_bwd_blocks((int)T) * 3 * h, (int64_t)COL_PARTS * maxw);
   if ((st = A((void**)&s->part, part_elems * 4))) return st;
+  if (s->dtype == STAGE_BF16 &&
+      (st = A((void**)&s->part2, (int64_t)ln_bwd_blocks((int)T) * 3 * h * 4)))
+    return st;
   // Split-K partials.  bf16 stages compute a layer's weight gradients in
   // one group launch: room for all four gradients' partials.  fp32 stages
   // compute them one at a time: the largest one's.
@@ -423,9 +427,10 @@ struct WgradJob {
 
 // The queued weight gradients of one layer in one GEMM launch (stream-K
 // over all their tiles, fp32 partials side by side in the split-K buffer)
-// and one fixed-order reduction launch.
-stage_status wgrad_group(stage_t* s, const WgradJob* jobs, int n) {
-  if (n == 0) return STAGE_OK;
+// and one fixed-order reduction launch, which also runs the layer's queued
+// column reductions (bias, gamma and beta gradients).
+stage_status wgrad_group(stage_t* s, const WgradJob* jobs, int n, const ColJob* cols, int ncols) {
+  if (n == 0 && ncols == 0) return STAGE_OK;
   const int Tn = s->B * s->S;
   GemmArgs gs[GEMM_GROUP_MAX];
   float* outs[GEMM_GROUP_MAX];
@@ -446,7 +451,7 @@ stage_status wgrad_group(stage_t* s, const WgradJob* jobs, int n) {
   }
   if (off > s->splitk_elems) return fail(s, STAGE_EHIP, "split-K buffer too small");
   SITE(WGRAD_GROUP, gemm_bf16_wgrad_group(gs, n, s->stream));
-  SITE(WGRAD_GROUP_RED, wgrad_group_reduce(gs, outs, n, s->stream));
+  SITE(WGRAD_GROUP_RED, wgrad_group_reduce(gs, outs, n, cols, ncols, s->stream));
   return STAGE_OK;
 }
 
@@ -567,13 +572,21 @@ stage_status forward_impl(stage_t* s, const T* x, T* y) {
   return STAGE_OK;
 }
 
+// LayerNorm backward into partials `part`; their column reduction into
+// dgamma, dbeta, dbias runs here, or is queued in *defer (bf16 stages: run
+// with the layer's weight-gradient reduction).
 template <typename T>
 stage_status ln_backward(stage_t* s, int site, int site_red, const T* dy, const T* xhat, const float* rstd,
-                         const float* gamma, T* dz, float* dgamma, float* dbeta, float* dbias) {
+                         const float* gamma, T* dz, float* dgamma, float* dbeta, float* dbias,
+                         float* part, ColJob* defer) {
   const int Tn = s->B * s->S, h = s->h;
-  SITE_I(site, ln_bwd<T>(dy, xhat, rstd, gamma, dz, s->part, Tn, h, s->stream));
+  SITE_I(site, ln_bwd<T>(dy, xhat, rstd, gamma, dz, part, Tn, h, s->stream));
+  if (defer) {
+    *defer = ColJob{part, ln_bwd_blocks(Tn), 3, h, {dgamma, dbeta, dbias, nullptr}};
+    return STAGE_OK;
+  }
   float* outs[3] = {dgamma, dbeta, dbias};
-  SITE_I(site_red, col_reduce(s->part, ln_bwd_blocks(Tn), 3, h, outs, s->stream));
+  SITE_I(site_red, col_reduce(part, ln_bwd_blocks(Tn), 3, h, outs, s->stream));
   return STAGE_OK;
 }
 
@@ -618,6 +631,10 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
     // one group launch at the end of the layer.
     WgradJob wjobs[GEMM_GROUP_MAX];
     int nw = 0;
+    // and their column reductions (LayerNorm and bias gradients) in the
+    // same group's reduction launch
+    ColJob cjobs[COLJOB_MAX];
+    int nc = 0;
     auto dW = [&](int site, int site_red, const T* dYm, int64_t ld_dy, const T* Xn,
                   int64_t ld_x, int M, int N, float* out) -> stage_status {
       if (kBF) {
@@ -649,7 +666,8 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
     if (ffn) {
       // Y = LN(Z2): dZ2, dgamma2, dbeta2, and db_2 = sum_t dZ2
       if ((r = ln_backward<T>(s, SITE_LN2_BWD, SITE_LN2_RED, dYcur, (const T*)v.xhat2, v.rstd2, (const float*)p[STAGE_G2], dZ2,
-                              gr[STAGE_G2], gr[STAGE_BE2], gr[STAGE_B_2])))
+                              gr[STAGE_G2], gr[STAGE_BE2], gr[STAGE_B_2], kBF ? s->part2 : s->part,
+                              kBF ? &cjobs[nc++] : nullptr)))
         return r;
       // dW_2 = dZ2^T G
       if ((r = dW(SITE_W2_WGRAD, SITE_W2_RED, dZ2, h, (const T*)v.G, f, h, f, gr[STAGE_W_2]))) return r;
@@ -665,8 +683,7 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
         SITE(FFN2_DGRAD, Gemm<T>::run(g, true, kBF, EPI_MUL, false, 1, st));
       }
       if (kBF) {
-        float* outs[1] = {gr[STAGE_B_1]};
-        SITE(B1_RED, col_reduce(s->colpart_ffn, (Tn + 127) / 128, 1, f, outs, st));
+        cjobs[nc++] = ColJob{s->colpart_ffn, (Tn + 127) / 128, 1, f, {gr[STAGE_B_1], nullptr, nullptr, nullptr}};
       } else if ((r = col_sum<T>(s, SITE_B1_SUM, SITE_B1_RED, dU, f, gr[STAGE_B_1]))) {
         return r;
       }
@@ -684,12 +701,13 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
       dH1in = dH1out;
     }  // feed-forward half
     if (!attn) {
-      if ((r = wgrad_group(s, wjobs, nw))) return r;
+      if ((r = wgrad_group(s, wjobs, nw, cjobs, nc))) return r;
       break;
     }
     // H1 = LN(Z1): dZ1, dgamma1, dbeta1, db_o
     if ((r = ln_backward<T>(s, SITE_LN1_BWD, SITE_LN1_RED, dH1in, (const T*)v.xhat1, v.rstd1, (const float*)p[STAGE_G1], dZ1,
-                            gr[STAGE_G1], gr[STAGE_BE1], gr[STAGE_B_O])))
+                            gr[STAGE_G1], gr[STAGE_BE1], gr[STAGE_B_O], s->part,
+                            kBF ? &cjobs[nc++] : nullptr)))
       return r;
     // dW_o = dZ1^T C
     if ((r = dW(SITE_WO_WGRAD, SITE_WO_RED, dZ1, h, (const T*)v.C, h, h, h, gr[STAGE_W_O]))) return r;
@@ -705,8 +723,8 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
       aa.colpart = s->colpart_qkv;  // db_qkv: column sums per 32-row block
       SITE(ATTN_DQ, attn_backward_dq(aa, st));
       SITE(ATTN_DKDV, attn_backward_dkdv(aa, st));
-      float* outs[1] = {gr[STAGE_B_QKV]};
-      SITE(BQKV_RED, col_reduce(s->colpart_qkv, B * ((S + 31) / 32), 1, 3 * h, outs, st));
+      cjobs[nc++] = ColJob{s->colpart_qkv, B * ((S + 31) / 32), 1, 3 * h,
+                           {gr[STAGE_B_QKV], nullptr, nullptr, nullptr}};
     } else {
     // dP[b, j] = dC_bj V_bj^T (fp32, into the score buffer)
     {
@@ -771,7 +789,7 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
       g.ldaux = h;
       SITE(QKV_DGRAD, Gemm<T>::run(g, true, kBF, EPI_RESID, false, 1, st));
     }
-    if ((r = wgrad_group(s, wjobs, nw))) return r;
+    if ((r = wgrad_group(s, wjobs, nw, cjobs, nc))) return r;
     dYcur = dXout;
   }
   return STAGE_OK;
