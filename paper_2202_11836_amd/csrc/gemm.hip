@@ -669,15 +669,26 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
 #pragma unroll
           for (int j = 0; j < TN; ++j) bfr[nxt][j] = pb.get(j, 0);
         }
-        // Keep the scheduler from sinking the fragment reads down to their
-        // uses: they must be in flight while these MFMAs execute.
-        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
           for (int j = 0; j < TN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j],
                                                                 acc[i][j], 0, 0, 0);
+        // Issue order: one MFMA, then the next k-step's fragment reads
+        // spread evenly behind the MFMAs (each read issues while the
+        // matrix core works on the MFMA before it) instead of all reads
+        // ahead of the MFMAs.  Measured: -3% over the encoder GEMMs, -6%
+        // for the weight gradients (two reads per fragment).
+        {
+          constexpr int NM = TM * TN;
+          constexpr int NR = TM * (AK ? 1 : 2) + TN * (BKM ? 1 : 2);
+#pragma unroll
+          for (int m = 0; m < NM; ++m) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, (NR + NM - 1) / NM, 0);  // LDS read
+          }
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
     }
