@@ -131,6 +131,17 @@ __device__ __forceinline__ bf16x8_t frag_tr(const char* tile, int col0, int rb, 
 // "vmcnt = 0 and lgkmcnt = 0" (gfx9 s_waitcnt encoding).
 __device__ __forceinline__ void wait_all() { __builtin_amdgcn_s_waitcnt(0x0070); }
 
+// The values of lanes l and l ^ 32 (as a pair, in either order) from one
+// v_permlane32_swap, which exchanges the upper half of its first operand
+// with the lower half of its second: no LDS round trip, unlike a shuffle.
+struct HalfPair {
+  float x, y;
+};
+__device__ __forceinline__ HalfPair half_pair(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return {__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+
 // Write a wavefront's 32 x 64 result, held transposed in two accumulators
 // (lane = row l % 32, registers = columns), to dst rows [row0, row0 + 32)
 // clipped to nrows: staged through the wavefront's LDS area (32 x LD) so
@@ -313,7 +324,10 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
           }
         }
       }
-      mblk = fmaxf(mblk, __shfl_xor(mblk, 32, 64));
+      {
+        const HalfPair pr = half_pair(mblk);
+        mblk = fmaxf(pr.x, pr.y);
+      }
       // The exponent offset m moves only when a block maximum exceeds it by
       // more than 8 (log2 units), so exp2(s - m) <= 256 and most blocks
       // skip rescaling the output accumulators (a wavefront-uniform test).
@@ -329,12 +343,11 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
         m = mn;
       }
       const float off = m == -INFINITY ? 0.0f : m;
-      float ps = 0.0f;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], c, -off));
-        ps += s[r];
-      }
+      for (int r = 0; r < 16; ++r) s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], c, -off));
+      float ps = s[0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) ps += s[r];
       lsum += ps;
       // O^T += V_sub^T P^T
 #pragma unroll
@@ -350,7 +363,8 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
       store_kfull(kfull[st ^ 1], nbias, tid);
     }
   }
-  const float ltot = lsum + __shfl_xor(lsum, 32, 64);
+  const HalfPair lp = half_pair(lsum);
+  const float ltot = lp.x + lp.y;
   const float inv = ltot > 0.0f ? 1.0f / ltot : 0.0f;
   if (hf == 0 && q0 + rr < S)
     a.lse[(int64_t)bh * S + q0 + rr] = ltot > 0.0f ? m + __log2f(ltot) : 0.0f;
@@ -414,7 +428,10 @@ __global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) dsum += (float)dof[ks][i] * (float)of[i];
   }
-  dsum += __shfl_xor(dsum, 32, 64);  // D = rowsum(dO * O) of query q
+  {
+    const HalfPair dp2 = half_pair(dsum);
+    dsum = dp2.x + dp2.y;  // D = rowsum(dO * O) of query q
+  }
   if (hf == 0 && q < S) a.dsum[(int64_t)bh * S + q] = dsum;
   const float lse_q = q < S ? a.lse[(int64_t)bh * S + q] : 0.0f;
 
@@ -503,17 +520,20 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
   const int kend = a.kext[b];
   const int key = k0 + rr;
   const bool kvalid = key < kend && a.mask[(int64_t)b * S + key] != 0;
-  const bool kall = __all(kvalid);  // none of this wavefront's 32 keys is masked
   const bool block_live = kb128 * 128 < kend;  // uniform over the block
   const int nqb = block_live ? (S + QB - 1) / QB : 0;
   const __amdgpu_buffer_rsrc_t rsQ = rows_rsrc(Qg, S, ld), rsD = rows_rsrc(dOg, S, h);
-  // threads 0-127 carry lse, 128-255 D of query block qb (rows past S: P = 0)
+  // threads 0-127 carry lse, 128-255 -D of query block qb (rows past S:
+  // P = 0)
   static_assert(2 * QB == 256, "one value per thread");
   auto rowval = [&](int qb) {
     const int qq = qb * QB + (tid & (QB - 1));
     if (tid < QB) return qq < S ? a.lse[(int64_t)bh * S + qq] : INFINITY;
-    return qq < S ? a.dsum[(int64_t)bh * S + qq] : 0.0f;
+    return qq < S ? -a.dsum[(int64_t)bh * S + qq] : -0.0f;
   };
+  // Initial score accumulator: 0, or -inf for a masked key (the lane's
+  // column), which makes its probabilities exp2(-inf) = 0.
+  const f32x16_t s0 = splat16(kvalid ? 0.0f : -INFINITY);
 
   if (nqb > 0) {
     rowv[0][tid / QB][tid & (QB - 1)] = rowval(0);
@@ -550,12 +570,12 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
       if (qb * QB + 32 * sub >= S) break;
       // S (32 queries x 32 keys) = Q_sub K^T;  dP - D = dO_sub V^T - D (the
       // accumulator starts at -D of each register's query)
-      f32x16_t s = zero16(), dp;
+      f32x16_t s = s0, dp;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const f32x4_t dv4 = *(const f32x4_t*)&rowv[st][1][32 * sub + 8 * g + 4 * hf];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) dp[4 * g + e] = -dv4[e];
+        for (int e = 0; e < 4; ++e) dp[4 * g + e] = dv4[e];
       }
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
@@ -568,8 +588,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = 4 * g + e;
-          float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, -lv[e]));
-          if (!kall) p = kvalid ? p : 0.0f;
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, -lv[e]));
           s[r] = p;
           dp[r] = p * dp[r];  // dS (unscaled)
         }
