@@ -226,8 +226,10 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const T* __restrict__ dy,
 }
 
 // bf16 LayerNorm backward with the rows kept as packed bf16 (unpacked where
-// used) and gamma in LDS, so that four wavefronts per SIMD fit: the same
-// arithmetic and partial rows as ln_bwd_kernel, twice the loads in flight.
+// used) and gamma in LDS: the same arithmetic and partial rows as
+// ln_bwd_kernel, twice the loads in flight.  Register budget: two
+// work-groups per CU (16384 rows of 32 per work-group are 512 work-groups,
+// two per CU), which keeps every per-column partial in registers.
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 __device__ __forceinline__ float bf_at(const u32x4_t& r, int k) {
@@ -235,7 +237,7 @@ __device__ __forceinline__ float bf_at(const u32x4_t& r, int k) {
 }
 
 template <int NC>
-__global__ __launch_bounds__(256, (NC <= 2 ? 3 : 1)) void ln_bwd_bf16_kernel(const bf16_t* __restrict__ dy,
+__global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(const bf16_t* __restrict__ dy,
                                                             const bf16_t* __restrict__ xhat,
                                                             const float* __restrict__ rstd,
                                                             const float* __restrict__ gamma,
