@@ -226,7 +226,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const T* __restrict__ dy,
 }
 
 // bf16 LayerNorm backward with the rows kept as packed bf16 (unpacked where
-// used) and gamma in LDS: the same arithmetic and partial rows as
+// used) and gamma in registers: the same arithmetic and partial rows as
 // ln_bwd_kernel, twice the loads in flight.  Register budget: two
 // work-groups per CU (16384 rows of 32 per work-group are 512 work-groups,
 // two per CU), which keeps every per-column partial in registers.
@@ -244,18 +244,19 @@ __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(con
                                                             bf16_t* __restrict__ dz,
                                                             float* __restrict__ part, int rows,
                                                             int h, int rpb) {
-  extern __shared__ float red[];  // [4 wavefronts][3][h], then gamma [h]
-  float* gsh = red + 12 * h;
+  extern __shared__ float red[];  // [4 wavefronts][3][h]
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int nchunk = h >> 3;
-  for (int c = threadIdx.x; c < h; c += 256) gsh[c] = gamma[c];
-  __syncthreads();
-  float pg[NC][8], pb[NC][8], pz[NC][8];
+  // gamma of the lane's columns, in registers for all rows
+  float pg[NC][8], pb[NC][8], pz[NC][8], gm[NC][8];
 #pragma unroll
-  for (int i = 0; i < NC; ++i)
+  for (int i = 0; i < NC; ++i) {
+    const int c = lane + 64 * i;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) pg[i][k] = pb[i][k] = pz[i][k] = 0.0f;
+    for (int k = 0; k < 8; ++k) pg[i][k] = pb[i][k] = pz[i][k] = gm[i][k] = 0.0f;
+    if (c < nchunk) load8(gamma + 8 * c, gm[i]);
+  }
   const int r0 = blockIdx.x * rpb;
   const int r1 = min(rows, r0 + rpb);
   const float inv_h = 1.0f / (float)h;
@@ -279,15 +280,12 @@ __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(con
     float sg[2] = {0.0f, 0.0f}, sgx[2] = {0.0f, 0.0f};
 #pragma unroll
     for (int i = 0; i < NC; ++i) {
-      const int c = lane + 64 * i;
-      const int cc = c < nchunk ? c : 0;
-      const f32x4_t g0 = *(const f32x4_t*)(gsh + 8 * cc), g1 = *(const f32x4_t*)(gsh + 8 * cc + 4);
 #pragma unroll
       for (int u = 0; u < 2; ++u)
 #pragma unroll
         for (int k = 0; k < 8; ++k) {
           const float d = bf_at(dr[u][i], k), x = bf_at(xr[u][i], k);
-          const float g = d * (k < 4 ? g0[k] : g1[k - 4]);
+          const float g = d * gm[i][k];
           sg[u] += g;
           sgx[u] += g * x;
           pg[i][k] += d * x;
@@ -309,7 +307,6 @@ __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(con
       for (int i = 0; i < NC; ++i) {
         const int c = lane + 64 * i;
         if (c < nchunk) {
-          const f32x4_t g0 = *(const f32x4_t*)(gsh + 8 * c), g1 = *(const f32x4_t*)(gsh + 8 * c + 4);
           u32x4_t o;
 #pragma unroll
           for (int k2 = 0; k2 < 4; ++k2) {
@@ -318,8 +315,7 @@ __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(con
             for (int e = 0; e < 2; ++e) {
               const int k = 2 * k2 + e;
               const float d = bf_at(dr[u][i], k), x = bf_at(xr[u][i], k);
-              const float gm = k < 4 ? g0[k] : g1[k - 4];
-              dd[e] = rs * (d * gm - sg[u] - x * sgx[u]);
+              dd[e] = rs * (d * gm[i][k] - sg[u] - x * sgx[u]);
             }
             o[k2] = pack_bf16x2(dd[0], dd[1]);
             // The column sum uses the value as stored, so that the bias
@@ -522,7 +518,6 @@ hipError_t ln_bwd(const T* dy, const T* xhat, const float* rstd, const float* ga
   size_t sh = (size_t)4 * 3 * h * sizeof(float);
   const int rpb = LN_BWD_RPB;
   if constexpr (std::is_same<T, bf16_t>::value) {
-    sh += (size_t)h * sizeof(float);
     switch (nc) {
       case 1: hipLaunchKernelGGL((ln_bwd_bf16_kernel<1>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
       case 2: hipLaunchKernelGGL((ln_bwd_bf16_kernel<2>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
