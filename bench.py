@@ -234,31 +234,31 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # Forward / backward split (paper reports them separately), untimed pass.
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-    fwd_ms = bwd_ms = 0.0
-    for _ in range(3):
-        ev[0].record()
-        st.forward(x, mask, out=y)
-        ev[1].record()
-        st.backward(dy, out=dx)
-        ev[2].record()
-        torch.cuda.synchronize()
-        fwd_ms += ev[0].elapsed_time(ev[1]) / 3
-        bwd_ms += ev[1].elapsed_time(ev[2]) / 3
-
-    # Timed region; the dominant kernel's launches are traced with HIP events
-    # on the stage stream.
+    # Timed region: exactly --steps steps.  Each step is bracketed by HIP
+    # events on the stage stream (torch's current stream), with one more
+    # between its forward and backward, so the per-step median and spread
+    # and the forward / backward split (the paper reports them separately)
+    # come from the same timed steps; the dominant kernel's launches are
+    # traced with HIP events on that stream as well.
     kernel_name, roof_sites = ROOFLINE_KERNELS[args.roofline_kernel]
     st.trace(roof_sites)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
+    for i in range(args.steps):
+        ev[i][0].record()
+        st.forward(x, mask, out=y)
+        ev[i][1].record()
+        st.backward(dy, out=dx)
+        ev[i][2].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     launches, site_ms = st.trace_read()
     st.trace(None)
+    fwd_s = np.array([e[0].elapsed_time(e[1]) for e in ev])
+    bwd_s = np.array([e[1].elapsed_time(e[2]) for e in ev])
+    step_s = np.array([e[0].elapsed_time(e[2]) for e in ev])
+    fwd_ms, bwd_ms = float(np.median(fwd_s)), float(np.median(bwd_s))
 
     ms_per_step = (t1 - t0) * 1000.0 / args.steps
     tokens = cfg.batch * cfg.seq
@@ -302,8 +302,14 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
+        "step_ms_median": float(np.median(step_s)),
+        "step_ms_spread": {"min": float(step_s.min()), "p10": float(np.percentile(step_s, 10)),
+                           "p90": float(np.percentile(step_s, 90)), "max": float(step_s.max())},
         "fwd_ms": fwd_ms,
         "bwd_ms": bwd_ms,
+        "timing": "value and ms_per_step: wall clock over the timed steps (mean); "
+                  "step_ms_median / spread, fwd_ms, bwd_ms: medians of per-step HIP events "
+                  "on the stage stream over the same steps",
         "tflops": tflops,
         "pct_bf16_peak": 100.0 * tflops / PEAK_BF16_TFLOPS,
         "higher_is_better": True,

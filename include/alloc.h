@@ -32,7 +32,19 @@
 extern "C" {
 #endif
 
-typedef enum {
+/* Enumerations are int-sized on both sides of the ABI.  Compiled as C++
+ * they get a fixed underlying type int, so that every int a C caller passes
+ * is a value of the type there too (and is rejected by the argument checks
+ * when it is not one of the listed values), instead of being undefined. */
+#ifndef SKY_ENUM_INT
+#ifdef __cplusplus
+#define SKY_ENUM_INT : int
+#else
+#define SKY_ENUM_INT
+#endif
+#endif
+
+typedef enum SKY_ENUM_INT {
   ALLOC_OK = 0,
   ALLOC_EINVAL = 1, /* L < D, D < 1, null pointer, non-finite or negative input,
                        malformed partition index */
@@ -41,7 +53,7 @@ typedef enum {
                        changing for L * D sweeps) */
 } alloc_status;
 
-typedef enum {
+typedef enum SKY_ENUM_INT {
   ALLOC_CT_PER_LAYER = 0, /* sum_j (dt[i] lf[j] + ct[i]), section IV-D */
   ALLOC_CT_PER_DEVICE = 1 /* dt[i] sum_j lf[j] + ct[i], section IV-C */
 } alloc_ct_mode;
@@ -80,6 +92,7 @@ alloc_status alloc_fine(int L, int D, const double* dt, const double* dm, const 
 
 /*
  * Workload of every device under partition pi: w_out[i] for i < D.
+ * EINVAL for a mode other than the two alloc_ct_mode values.
  * Rejects a pi that is not 0 = pi[0] < pi[1] < ... < pi[D] = L.
  */
 alloc_status alloc_workloads(int L, int D, const double* dt, const double* ct, const double* lf,

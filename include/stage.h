@@ -39,9 +39,21 @@
 extern "C" {
 #endif
 
+/* Enumerations are int-sized on both sides of the ABI.  Compiled as C++
+ * they get a fixed underlying type int, so that every int a C caller passes
+ * is a value of the type there too (and is rejected by the argument checks
+ * when it is not one of the listed values), instead of being undefined. */
+#ifndef SKY_ENUM_INT
+#ifdef __cplusplus
+#define SKY_ENUM_INT : int
+#else
+#define SKY_ENUM_INT
+#endif
+#endif
+
 typedef struct stage stage_t; /* opaque, library-owned */
 
-typedef enum {
+typedef enum SKY_ENUM_INT {
   STAGE_OK = 0,
   STAGE_EINVAL = 1, /* invalid argument: dims, null pointer, index range */
   STAGE_ESTATE = 2, /* call out of order, e.g. backward without forward */
@@ -49,9 +61,9 @@ typedef enum {
   STAGE_EHIP = 4    /* a HIP runtime call or kernel launch failed */
 } stage_status;
 
-typedef enum { STAGE_F32 = 0, STAGE_BF16 = 1 } stage_dtype;
+typedef enum SKY_ENUM_INT { STAGE_F32 = 0, STAGE_BF16 = 1 } stage_dtype;
 
-typedef enum {
+typedef enum SKY_ENUM_INT {
   STAGE_W_QKV = 0, /* [3h, h]  dtype */
   STAGE_B_QKV = 1, /* [3h]     fp32  */
   STAGE_W_O = 2,   /* [h, h]   dtype */
@@ -68,7 +80,7 @@ typedef enum {
 } stage_param_id;
 
 /* Saved activations of the latest forward pass (for layer-wise checks). */
-typedef enum {
+typedef enum SKY_ENUM_INT {
   STAGE_SAVED_X = 0,   /* layer input           [T, h]  dtype */
   STAGE_SAVED_QKV = 1, /* Q | K | V             [T, 3h] dtype */
   STAGE_SAVED_CTX = 2, /* attention context     [T, h]  dtype */
@@ -109,9 +121,12 @@ stage_status stage_init(int L_stage, int hidden, int heads, int ffn, uint64_t se
  * stage_read, ...  Its input is X of its first unit's layer (H1 when
  * first_unit is odd) and its output is that of its last unit.  Chaining the
  * stages of a partition of [0, 2 L) computes the same function as one stage
- * of L layers, except that on bf16 stages an H1 that crosses a stage
- * boundary reaches the second LayerNorm rounded to bf16 (inside a stage it
- * is added in fp32).  Weights are drawn as in stage_init with the global
+ * of L layers, except that on bf16 stages the tensors that cross a stage
+ * boundary are rounded to bf16 there (they are the stage's input and output
+ * in its dtype): an H1 that crosses a boundary reaches the second LayerNorm
+ * rounded (inside a stage it is added in fp32), and in the backward pass the
+ * gradient that crosses a boundary is rounded (inside a stage the residual
+ * stream of the backward pass stays in fp32).  Weights are drawn as in stage_init with the global
  * layer index, so a layer has the same weights in every stage that holds
  * it; stage_init(L, ...) is stage_init_units(0, 2 L, ...).  Parameters,
  * gradients and saved tensors of the absent half of a partial layer do not
@@ -174,11 +189,24 @@ stage_status stage_memory_model_units(int hidden, int heads, int ffn, int batch,
                                       stage_dtype dtype, int64_t* attn_unit, int64_t* ffn_unit,
                                       int64_t* shared);
 
-/* Device pointer, element count and dtype of parameter `which` of `layer`. */
+/*
+ * Device pointer, element count and dtype of parameter `which` of `layer`.
+ * Section III: each device holds the weights of its own layers for the
+ * whole of training (fetched once at the start) and updates them locally;
+ * the pointer stays valid until stage_destroy, so the caller's optimiser can
+ * update the weights in place between steps.  EINVAL for an index out of
+ * range or a half-layer the stage does not hold.
+ */
 stage_status stage_param(stage_t* s, int layer, int which, void** dev_ptr, int64_t* numel,
                          stage_dtype* dtype);
 
-/* Device pointer (fp32) and element count of that parameter's gradient. */
+/*
+ * Device pointer (fp32) and element count of that parameter's gradient.
+ * Section III: after its backward pass a device uses the gradients of its
+ * own layers to update their weights locally; they are never sent to
+ * another device.  Overwritten by every stage_backward; valid until
+ * stage_destroy.  Errors as stage_param.
+ */
 stage_status stage_grad(stage_t* s, int layer, int which, float** dev_ptr, int64_t* numel);
 
 /*
@@ -191,10 +219,23 @@ stage_status stage_set_param(stage_t* s, int layer, int which, const void* src, 
 /*
  * Copy a library-owned tensor into dst (host or device), synchronously on
  * the stage stream.  kind 0 = parameter, 1 = gradient, 2 = saved activation
- * (stage_saved_id; needs a saved context).  bytes must equal the tensor's
+ * (stage_saved_id; needs a saved context), 3 = the gradient that reached
+ * layer `layer`'s output in the latest backward (which = 0; fp32 [T, h];
+ * needs stage_record_grads, else ESTATE).  bytes must equal the tensor's
  * size in bytes (fp32 for gradients).
  */
 stage_status stage_read(stage_t* s, int kind, int layer, int which, void* dst, size_t bytes);
+
+/*
+ * Record, in every later backward, the gradient that reaches each layer's
+ * output (section III: the gradients flow through the layers in reverse
+ * order; on bf16 stages this is the fp32 residual stream inside the stage),
+ * for layer-wise checks through stage_read kind 3.  on = 1 or 0.  Takes
+ * effect at the next stage_forward, which (re)allocates T * h * 4 bytes per
+ * layer for the record (or frees it); the current saved context is
+ * dropped.  EINVAL for other values of on.
+ */
+stage_status stage_record_grads(stage_t* s, int on);
 
 /* Bytes of the tensor stage_read(kind, layer, which) would copy (0 if none). */
 size_t stage_tensor_bytes(stage_t* s, int kind, int layer, int which);

@@ -20,7 +20,7 @@ STAGE_F32, STAGE_BF16 = 0, 1
 PARAM_NAMES = ("W_qkv", "b_qkv", "W_o", "b_o", "g1", "be1",
                "W_1", "b_1", "W_2", "b_2", "g2", "be2")
 SAVED_NAMES = ("X", "QKV", "CTX", "H1", "GD", "G")  # GD = GELU'(U)
-KIND_PARAM, KIND_GRAD, KIND_SAVED = 0, 1, 2
+KIND_PARAM, KIND_GRAD, KIND_SAVED, KIND_RECORDED_GRAD = 0, 1, 2, 3
 STATUS_NAMES = {0: "OK", 1: "EINVAL", 2: "ESTATE", 3: "ENOMEM", 4: "EHIP"}
 
 ALLOC_OK, ALLOC_EINVAL, ALLOC_ENOFIT = range(3)
@@ -32,7 +32,7 @@ EXPORTED = ("alloc_coarse", "alloc_fine", "alloc_workloads", "stage_init", "stag
             "stage_grad", "stage_set_param", "stage_read", "stage_tensor_bytes",
             "stage_trace_site", "stage_trace_mask", "stage_trace_read", "stage_site_count",
             "stage_site_name", "stage_device_bytes", "stage_memory_model",
-            "stage_memory_model_units", "stage_mfma_peak",
+            "stage_memory_model_units", "stage_mfma_peak", "stage_record_grads",
             "stage_last_error", "stage_destroy")
 
 _lib = None
@@ -109,6 +109,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.stage_mfma_peak.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_double),
                                     ctypes.POINTER(ctypes.c_double)]
     lib.stage_mfma_peak.restype = i32
+    lib.stage_record_grads.argtypes = [vp, i32]
+    lib.stage_record_grads.restype = i32
     dp, ip = ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)
     lib.alloc_coarse.argtypes = [i32, i32, dp, dp, ip, ip]
     lib.alloc_coarse.restype = i32
@@ -198,6 +200,10 @@ def stage_set_param(handle, layer: int, which: int, src) -> None:
 def stage_read(handle, kind: int, layer: int, which: int, dst) -> None:
     nbytes = dst.numel() * dst.element_size()
     _check(handle, load_library().stage_read(handle, kind, layer, which, dst.data_ptr(), nbytes))
+
+
+def stage_record_grads(handle, on: int) -> None:
+    _check(handle, load_library().stage_record_grads(handle, int(on)))
 
 
 def stage_tensor_bytes(handle, kind: int, layer: int, which: int) -> int:
@@ -353,6 +359,20 @@ class Stage:
         out = torch.empty((tokens, width), dtype=self.torch_dtype, device="cuda")
         self._sync_stream()
         stage_read(self.handle, KIND_SAVED, layer, which, out)
+        return out
+
+    def record_grads(self, on: bool = True):
+        """Record the gradient reaching each layer's output in later
+        backward passes (from the next forward on)."""
+        stage_record_grads(self.handle, 1 if on else 0)
+
+    def recorded_grad(self, layer: int, tokens: int):
+        """fp32 [tokens, hidden] gradient that reached `layer`'s output in
+        the latest backward."""
+        import torch
+        out = torch.empty((tokens, self.hidden), dtype=torch.float32, device="cuda")
+        self._sync_stream()
+        stage_read(self.handle, KIND_RECORDED_GRAD, layer, 0, out)
         return out
 
     def trace(self, site_names):

@@ -65,5 +65,77 @@ def build(verbose: bool = False) -> str:
     return LIB_PATH
 
 
+# Host code with AddressSanitizer and UndefinedBehaviorSanitizer (device
+# code unchanged): each sanitizer flag applies to the host compilation only.
+SAN_HOST = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer"]
+SAN_DIR = os.path.join(BUILD_DIR, "sanitized")
+SAN_LIB = os.path.join(SAN_DIR, "libskystage_sanitized.so")
+
+
+def _hash_sources() -> str:
+    import hashlib
+    hsh = hashlib.sha256()
+    for src in _sources() + [os.path.join(os.path.dirname(PKG), "include", f)
+                             for f in sorted(os.listdir(os.path.join(os.path.dirname(PKG), "include")))]:
+        hsh.update(src.encode())
+        hsh.update(open(src, "rb").read())
+    for f in sorted(os.listdir(CSRC)):
+        if f.endswith(".h"):
+            hsh.update(open(os.path.join(CSRC, f), "rb").read())
+    return hsh.hexdigest()
+
+
+def sanitizer_runtime() -> str:
+    """The AddressSanitizer runtime of the compiler hipcc drives (the
+    process that loads the sanitized library must preload it)."""
+    clang = os.path.join(os.path.dirname(os.path.realpath(HIPCC)), "..", "lib", "llvm", "bin", "clang")
+    if not os.path.exists(clang):
+        clang = "/opt/rocm/lib/llvm/bin/clang"
+    r = subprocess.run([clang, "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True,
+                       text=True)
+    path = r.stdout.strip()
+    if r.returncode != 0 or not os.path.isabs(path) or not os.path.exists(path):
+        rd = subprocess.run([clang, "--print-runtime-dir"], capture_output=True, text=True).stdout.strip()
+        path = os.path.join(rd, "libclang_rt.asan-x86_64.so")
+    if not os.path.exists(path):
+        raise RuntimeError("AddressSanitizer runtime not found")
+    return path
+
+
+def build_sanitized() -> str:
+    """Build libskystage_sanitized.so (host code under ASan + UBSan) into
+    _build/sanitized; reused while the sources are unchanged."""
+    os.makedirs(SAN_DIR, exist_ok=True)
+    stamp = os.path.join(SAN_DIR, "sources.sha256")
+    digest = _hash_sources()
+    if os.path.exists(SAN_LIB) and os.path.exists(stamp) and open(stamp).read() == digest:
+        return SAN_LIB
+
+    def comp(src):
+        base, ext = os.path.splitext(os.path.basename(src))
+        obj = os.path.join(SAN_DIR, base + ext.replace(".", "_") + ".o")
+        if ext == ".cpp":
+            cmd = [HIPCC, "-O1", "-g", "-std=c++17", "-fPIC"] + SAN_HOST + ["-c", src, "-o", obj]
+        else:
+            cmd = [HIPCC] + COMMON_FLAGS[:1] + ["-O1", "-g"] + COMMON_FLAGS[2:] + SAN_HOST + [
+                "-c", src, "-o", obj]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"sanitized build failed for {src}:\n{r.stderr}")
+        return obj
+
+    srcs = _sources()
+    with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        objs = list(ex.map(comp, srcs))
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC"] + SAN_HOST + ["-o", SAN_LIB] + objs
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized link failed:\n{r.stderr}")
+    with open(stamp, "w") as fh:
+        fh.write(digest)
+    return SAN_LIB
+
+
 if __name__ == "__main__":
     build(verbose=True)

@@ -62,6 +62,18 @@ __device__ __forceinline__ bf16x8_t pack8(const f32x16_t& a, int r0) {
   return __builtin_bit_cast(bf16x8_t, w);
 }
 
+// The bf16 rounding residuals a[r] - hi[r] of registers r0 .. r0+7, where
+// hi = pack8(a, r0), as a bf16 operand.
+__device__ __forceinline__ bf16x8_t pack8_residual(const f32x16_t& a, int r0, bf16x8_t hi) {
+  const u32x4_t h = __builtin_bit_cast(u32x4_t, hi);
+  u32x4_t w;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    w[i] = pack_bf16x2(a[r0 + 2 * i] - __uint_as_float(h[i] << 16),
+                       a[r0 + 2 * i + 1] - __uint_as_float(h[i] & 0xffff0000u));
+  return __builtin_bit_cast(bf16x8_t, w);
+}
+
 __device__ __forceinline__ bf16x8_t ld_frag(const bf16_t* p) { return *(const bf16x8_t*)p; }
 
 __device__ __forceinline__ u32x4_t zero4() { return u32x4_t{0, 0, 0, 0}; }
@@ -147,9 +159,15 @@ __device__ __forceinline__ HalfPair half_pair(float v) {
 // clipped to nrows: staged through the wavefront's LDS area (32 x LD) so
 // that the global stores are 16-byte row segments.  If colsum is not null it
 // receives the 64 column sums of the stored (bf16) values of those rows.
+// With residual, the values stored are the bf16 rounding residuals
+// v - bf16(v) of the scaled accumulators (rounded to bf16 in turn), so that
+// the pair (stored, residual) holds v to about 16 significant bits.
+__device__ __forceinline__ float bf16_residual(float v) {
+  return v - __uint_as_float(pack_bf16x2(v, v) << 16);
+}
 __device__ __forceinline__ void store_rows_t(const f32x16_t acc[2], float mul, bf16_t* stage,
                                              bf16_t* __restrict__ dst, int64_t ld, int row0,
-                                             int nrows, float* colsum) {
+                                             int nrows, float* colsum, bool residual = false) {
   const int lane = threadIdx.x & 63, hf = lane >> 5, rr = lane & 31;
 #pragma unroll
   for (int t = 0; t < 2; ++t)
@@ -157,8 +175,14 @@ __device__ __forceinline__ void store_rows_t(const f32x16_t acc[2], float mul, b
     for (int q = 0; q < 4; ++q) {
       // registers 4q .. 4q+3 are 4 consecutive columns
       const int col = 32 * t + 8 * q + 4 * hf;
-      const uint32_t lo = pack_bf16x2(acc[t][4 * q] * mul, acc[t][4 * q + 1] * mul);
-      const uint32_t hi = pack_bf16x2(acc[t][4 * q + 2] * mul, acc[t][4 * q + 3] * mul);
+      float v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[e] = acc[t][4 * q + e] * mul;
+        if (residual) v[e] = bf16_residual(v[e]);
+      }
+      const uint32_t lo = pack_bf16x2(v[0], v[1]);
+      const uint32_t hi = pack_bf16x2(v[2], v[3]);
       *(u32x2_t*)(stage + rr * LD + col) = u32x2_t{lo, hi};
     }
   __builtin_amdgcn_s_waitcnt(0);
@@ -349,13 +373,20 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
 #pragma unroll
       for (int r = 1; r < 16; ++r) ps += s[r];
       lsum += ps;
-      // O^T += V_sub^T P^T
+      // O^T += V_sub^T P^T, P as its bf16 value plus its bf16 rounding
+      // residual (two MFMAs on one V fragment): the context then carries
+      // about 16 significant bits of P, which the backward's D = rowsum(dO
+      // O) needs to match the rows of P dP it is subtracted from.
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         const bf16x8_t pb = pack8(s, 8 * ks);
+        const bf16x8_t pl = pack8_residual(s, 8 * ks, pb);
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
-          acc[t] = mfma32(frag_tr(Vs, 32 * t, 32 * sub + 16 * ks, lane), pb, acc[t]);
+        for (int t = 0; t < 2; ++t) {
+          const bf16x8_t vf = frag_tr(Vs, 32 * t, 32 * sub + 16 * ks, lane);
+          acc[t] = mfma32(vf, pb, acc[t]);
+          acc[t] = mfma32(vf, pl, acc[t]);
+        }
       }
     }
     if (kb + 1 < nkb && tid < KT) {
@@ -371,6 +402,11 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
   __syncthreads();  // the ring becomes the output staging area
   bf16_t* stage = (bf16_t*)&tiles[0][0] + wave * 32 * LD;
   store_rows_t(acc, inv, stage, a.out + (int64_t)b * S * h + j * HD, h, q0, S, nullptr);
+  if (a.out_lo) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_wave_barrier();
+    store_rows_t(acc, inv, stage, a.out_lo + (int64_t)b * S * h + j * HD, h, q0, S, nullptr, true);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -412,21 +448,26 @@ __global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
     dma_rows(rsK, 0, ld, tiles[0], wave, lane);
     dma_rows(rsV, 0, ld, tiles[0] + TILE, wave, lane);
   }
+  // D = rowsum(dO * O) with O = the stored context plus its rounding
+  // residual: the rows of dS = P (dP - D) then sum to zero up to fp32 and
+  // residual rounding, as the key-bias gradient (exactly zero) requires.
+  const bf16_t* __restrict__ Olg = a.o_lo ? a.o_lo + (int64_t)b * S * h + j * HD : nullptr;
   bf16x8_t qf[4], dof[4];
   float dsum = 0.0f;
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
     const int c = 16 * ks + 8 * hf;
-    bf16x8_t of;
+    bf16x8_t of, olf;
     if (q < S) {
       qf[ks] = ld_frag(Qg + (int64_t)q * ld + c);
       dof[ks] = ld_frag(dOg + (int64_t)q * h + c);
       of = ld_frag(Og + (int64_t)q * h + c);
+      olf = Olg ? ld_frag(Olg + (int64_t)q * h + c) : __builtin_bit_cast(bf16x8_t, zero4());
     } else {
-      qf[ks] = dof[ks] = of = __builtin_bit_cast(bf16x8_t, zero4());
+      qf[ks] = dof[ks] = of = olf = __builtin_bit_cast(bf16x8_t, zero4());
     }
 #pragma unroll
-    for (int i = 0; i < 8; ++i) dsum += (float)dof[ks][i] * (float)of[i];
+    for (int i = 0; i < 8; ++i) dsum += (float)dof[ks][i] * ((float)of[i] + (float)olf[i]);
   }
   {
     const HalfPair dp2 = half_pair(dsum);

@@ -126,6 +126,16 @@ template <typename T>
 hipError_t ln_bwd(const T* dy, const T* xhat, const float* rstd, const float* gamma, T* dz,
                   float* part, int rows, int h, hipStream_t st);
 
+// bf16 stages: the same with dy either one bf16 tensor (dya = dyb = null)
+// or the fp32 sum dya + dyb (dy = null); dz in bf16 and, when dz32 is not
+// null, in fp32 as well.  Partials as ln_bwd.
+hipError_t ln_bwd_bf16(const bf16_t* dy, const float* dya, const float* dyb, const bf16_t* xhat,
+                       const float* rstd, const float* gamma, bf16_t* dz, float* dz32,
+                       float* part, int rows, int h, hipStream_t st);
+// out = bf16(a + b), n elements (a multiple of 8).
+hipError_t add_f32_to_bf16(const float* a, const float* b, bf16_t* out, int64_t n,
+                           hipStream_t st);
+
 // dst[c][r] = src[r][c] for a bf16 [R][C] matrix.
 // dst[c][r] = src[r][c] for up to TRANSPOSE_MAX_JOBS row-major R x C bf16
 // matrices in one launch (R, C multiples of 8; tile0 is filled in).
@@ -168,6 +178,7 @@ hipError_t softmax_bwd(const float* dP, const T* P, T* dS, int BH, int S, int ld
 //   out:  forward: context [B*S, h]; backward: dQKV [B*S, 3h]
 //   lse:  [B*H, S] fp32 log2-sum-exp of the scaled scores (forward output)
 //   o, dout: forward context and its gradient [B*S, h] (backward inputs)
+//   out_lo / o_lo: the context's bf16 rounding residual [B*S, h]
 //   dsum: [B*H, S] fp32 rowsum(dO * O) (written by attn_backward_dq)
 // ---------------------------------------------------------------------------
 struct AttnArgs {
@@ -181,6 +192,11 @@ struct AttnArgs {
   float* lse;
   const bf16_t* o;
   const bf16_t* dout;
+  // forward, optional: the bf16 rounding residual of the context, out_lo =
+  // bf16(C - bf16(C)) with C the fp32 context; backward, optional: the same
+  // tensor, added to o where D = rowsum(dO * O) is formed
+  bf16_t* out_lo;
+  const bf16_t* o_lo;
   float* dsum;
   int B, S, H, h;
   float scale_log2;  // softmax scale * log2(e)

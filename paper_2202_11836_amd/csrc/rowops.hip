@@ -236,14 +236,18 @@ __device__ __forceinline__ float bf_at(const u32x4_t& r, int k) {
   return (k & 1) ? bf_hi(r[k >> 1]) : bf_lo(r[k >> 1]);
 }
 
-template <int NC>
-__global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(const bf16_t* __restrict__ dy,
-                                                            const bf16_t* __restrict__ xhat,
-                                                            const float* __restrict__ rstd,
-                                                            const float* __restrict__ gamma,
-                                                            bf16_t* __restrict__ dz,
-                                                            float* __restrict__ part, int rows,
-                                                            int h, int rpb) {
+// The incoming gradient dy is either one bf16 tensor or, when SUM32, the
+// sum of two fp32 tensors dya + dyb (the backward residual stream of a bf16
+// stage: the fp32 gradient of the residual branch plus the fp32 product of
+// the data-gradient GEMM, so that the stream is never rounded to bf16).
+// dz goes out in bf16 (the operand of the following GEMMs) and, when dz32
+// is not null, in fp32 as well (the residual branch of the next addition).
+template <int NC, bool SUM32>
+__global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(
+    const bf16_t* __restrict__ dy, const float* __restrict__ dya, const float* __restrict__ dyb,
+    const bf16_t* __restrict__ xhat, const float* __restrict__ rstd,
+    const float* __restrict__ gamma, bf16_t* __restrict__ dz, float* __restrict__ dz32,
+    float* __restrict__ part, int rows, int h, int rpb) {
   extern __shared__ float red[];  // [4 wavefronts][3][h]
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
@@ -261,7 +265,9 @@ __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(con
   const int r1 = min(rows, r0 + rpb);
   const float inv_h = 1.0f / (float)h;
   for (int row0 = r0 + wave; row0 < r1; row0 += 8) {
+    // SUM32: dy as fp32 (two 16-byte halves of each addend); else packed bf16
     u32x4_t dr[2][NC], xr[2][NC];
+    f32x4_t fa[2][NC][2], fb[2][NC][2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int row = row0 + 4 * u;
@@ -270,13 +276,32 @@ __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(con
       for (int i = 0; i < NC; ++i) {
         const int c = lane + 64 * i;
         if (c < nchunk && row < r1) {
-          dr[u][i] = *(const u32x4_t*)(dy + base + 8 * c);
+          if constexpr (SUM32) {
+            fa[u][i][0] = *(const f32x4_t*)(dya + base + 8 * c);
+            fa[u][i][1] = *(const f32x4_t*)(dya + base + 8 * c + 4);
+            fb[u][i][0] = *(const f32x4_t*)(dyb + base + 8 * c);
+            fb[u][i][1] = *(const f32x4_t*)(dyb + base + 8 * c + 4);
+          } else {
+            dr[u][i] = *(const u32x4_t*)(dy + base + 8 * c);
+          }
           xr[u][i] = *(const u32x4_t*)(xhat + base + 8 * c);
         } else {
-          dr[u][i] = xr[u][i] = u32x4_t{0, 0, 0, 0};
+          if constexpr (SUM32) {
+            fa[u][i][0] = fa[u][i][1] = fb[u][i][0] = fb[u][i][1] = f32x4_t{0, 0, 0, 0};
+          } else {
+            dr[u][i] = u32x4_t{0, 0, 0, 0};
+          }
+          xr[u][i] = u32x4_t{0, 0, 0, 0};
         }
       }
     }
+    // the incoming gradient at (u, i, k)
+    auto dyv = [&](int u, int i, int k) -> float {
+      if constexpr (SUM32)
+        return fa[u][i][k >> 2][k & 3] + fb[u][i][k >> 2][k & 3];
+      else
+        return bf_at(dr[u][i], k);
+    };
     float sg[2] = {0.0f, 0.0f}, sgx[2] = {0.0f, 0.0f};
 #pragma unroll
     for (int i = 0; i < NC; ++i) {
@@ -284,7 +309,7 @@ __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(con
       for (int u = 0; u < 2; ++u)
 #pragma unroll
         for (int k = 0; k < 8; ++k) {
-          const float d = bf_at(dr[u][i], k), x = bf_at(xr[u][i], k);
+          const float d = dyv(u, i, k), x = bf_at(xr[u][i], k);
           const float g = d * gm[i][k];
           sg[u] += g;
           sgx[u] += g * x;
@@ -307,24 +332,25 @@ __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(con
       for (int i = 0; i < NC; ++i) {
         const int c = lane + 64 * i;
         if (c < nchunk) {
+          float dd[8];
+#pragma unroll
+          for (int k = 0; k < 8; ++k)
+            dd[k] = rs * (dyv(u, i, k) * gm[i][k] - sg[u] - bf_at(xr[u][i], k) * sgx[u]);
           u32x4_t o;
 #pragma unroll
           for (int k2 = 0; k2 < 4; ++k2) {
-            float dd[2];
-#pragma unroll
-            for (int e = 0; e < 2; ++e) {
-              const int k = 2 * k2 + e;
-              const float d = bf_at(dr[u][i], k), x = bf_at(xr[u][i], k);
-              dd[e] = rs * (d * gm[i][k] - sg[u] - x * sgx[u]);
-            }
-            o[k2] = pack_bf16x2(dd[0], dd[1]);
+            o[k2] = pack_bf16x2(dd[2 * k2], dd[2 * k2 + 1]);
             // The column sum uses the value as stored, so that the bias
             // gradient of the preceding linear layer matches the gradient
-            // that flows on.
+            // its weight gradient is formed from.
             pz[i][2 * k2] += bf_lo(o[k2]);
             pz[i][2 * k2 + 1] += bf_hi(o[k2]);
           }
           *(u32x4_t*)(dz + base + 8 * c) = o;
+          if (dz32) {
+            *(f32x4_t*)(dz32 + base + 8 * c) = f32x4_t{dd[0], dd[1], dd[2], dd[3]};
+            *(f32x4_t*)(dz32 + base + 8 * c + 4) = f32x4_t{dd[4], dd[5], dd[6], dd[7]};
+          }
         }
       }
     }
@@ -347,6 +373,20 @@ __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(con
   float* P = part + (int64_t)blockIdx.x * 3 * h;
   for (int e = threadIdx.x; e < 3 * h; e += 256)
     P[e] = ((red[e] + red[3 * h + e]) + red[6 * h + e]) + red[9 * h + e];
+}
+
+// out = a + b rounded to bf16, 8 elements per thread (n % 8 == 0).
+__global__ __launch_bounds__(256) void add_f32_to_bf16_kernel(const float* __restrict__ a,
+                                                              const float* __restrict__ b,
+                                                              bf16_t* __restrict__ out, int64_t n8) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n8) return;
+  float va[8], vb[8];
+  load8(a + 8 * i, va);
+  load8(b + 8 * i, vb);
+#pragma unroll
+  for (int k = 0; k < 8; ++k) va[k] += vb[k];
+  store8(out + 8 * i, va);
 }
 
 template <typename T>
@@ -508,6 +548,48 @@ hipError_t add_ln_fwd(const TA* a, const float* bias, const TR* resid, const flo
 
 int ln_bwd_blocks(int rows) { return (rows + LN_BWD_RPB - 1) / LN_BWD_RPB; }
 
+hipError_t ln_bwd_bf16(const bf16_t* dy, const float* dya, const float* dyb, const bf16_t* xhat,
+                       const float* rstd, const float* gamma, bf16_t* dz, float* dz32,
+                       float* part, int rows, int h, hipStream_t st) {
+  if (h % 64 != 0 || h > 2048) return hipErrorInvalidValue;
+  if ((dy == nullptr) == (dya == nullptr || dyb == nullptr)) return hipErrorInvalidValue;
+  if (rows <= 0) return hipSuccess;
+  const int nc = (h / 8 + 63) / 64;
+  dim3 grid(ln_bwd_blocks(rows)), blk(256);
+  size_t sh = (size_t)4 * 3 * h * sizeof(float);
+  const int rpb = LN_BWD_RPB;
+#define LAUNCH_LNB(NCV, S32)                                                                  \
+  hipLaunchKernelGGL((ln_bwd_bf16_kernel<NCV, S32>), grid, blk, sh, st, dy, dya, dyb, xhat, rstd, \
+                     gamma, dz, dz32, part, rows, h, rpb)
+  if (dy) {
+    switch (nc) {
+      case 1: LAUNCH_LNB(1, false); break;
+      case 2: LAUNCH_LNB(2, false); break;
+      case 3: LAUNCH_LNB(3, false); break;
+      default: LAUNCH_LNB(4, false); break;
+    }
+  } else {
+    switch (nc) {
+      case 1: LAUNCH_LNB(1, true); break;
+      case 2: LAUNCH_LNB(2, true); break;
+      case 3: LAUNCH_LNB(3, true); break;
+      default: LAUNCH_LNB(4, true); break;
+    }
+  }
+#undef LAUNCH_LNB
+  return hipGetLastError();
+}
+
+hipError_t add_f32_to_bf16(const float* a, const float* b, bf16_t* out, int64_t n,
+                           hipStream_t st) {
+  if (n % 8 != 0) return hipErrorInvalidValue;
+  const int64_t n8 = n / 8;
+  if (n8 == 0) return hipSuccess;
+  hipLaunchKernelGGL(add_f32_to_bf16_kernel, dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0, st,
+                     a, b, out, n8);
+  return hipGetLastError();
+}
+
 template <typename T>
 hipError_t ln_bwd(const T* dy, const T* xhat, const float* rstd, const float* gamma, T* dz,
                   float* part, int rows, int h, hipStream_t st) {
@@ -518,13 +600,7 @@ hipError_t ln_bwd(const T* dy, const T* xhat, const float* rstd, const float* ga
   size_t sh = (size_t)4 * 3 * h * sizeof(float);
   const int rpb = LN_BWD_RPB;
   if constexpr (std::is_same<T, bf16_t>::value) {
-    switch (nc) {
-      case 1: hipLaunchKernelGGL((ln_bwd_bf16_kernel<1>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
-      case 2: hipLaunchKernelGGL((ln_bwd_bf16_kernel<2>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
-      case 3: hipLaunchKernelGGL((ln_bwd_bf16_kernel<3>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
-      default: hipLaunchKernelGGL((ln_bwd_bf16_kernel<4>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
-    }
-    return hipGetLastError();
+    return ln_bwd_bf16(dy, nullptr, nullptr, xhat, rstd, gamma, dz, nullptr, part, rows, h, st);
   }
   switch (nc) {
     case 1: hipLaunchKernelGGL((ln_bwd_kernel<T, 1>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;

@@ -83,6 +83,14 @@ __global__ void fill_kernel(float* out, int64_t n, float v) {
   if (i < n) out[i] = v;
 }
 
+// out = bf (bf16) or a + b (fp32), as fp32.
+__global__ void grad_record_kernel(const bf16_t* bf, const float* a, const float* b, float* out,
+                                   int64_t n) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  out[i] = bf ? bf2f(bf[i]) : a[i] + (b ? b[i] : 0.0f);
+}
+
 __global__ void ones_u8_kernel(uint8_t* out, int64_t n) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) out[i] = 1;
@@ -102,6 +110,7 @@ struct Saved {
   void* P = nullptr;     // softmax probabilities [B*H, S, S] (fp32 stages)
   float* lse = nullptr;  // log2-sum-exp of the scaled scores [B*H, S] (bf16 stages)
   void* C = nullptr;     // context [T, h]
+  void* Clo = nullptr;   // its bf16 rounding residual [T, h] (bf16 stages)
   void* xhat1 = nullptr; // [T, h]
   float* rstd1 = nullptr;
   void* H1 = nullptr;    // [T, h]
@@ -151,7 +160,9 @@ struct stage {
   void* dH1 = nullptr;      // [T, h]
   void* dZ1 = nullptr;      // [T, h]
   void* dC = nullptr;       // [T, h]
-  void* dY = nullptr;       // [T, h] gradient flowing between layers
+  void* dY = nullptr;       // [T, h] gradient flowing between layers (fp32 stages)
+  float* dz1f = nullptr;    // [T, h] fp32 dZ1, residual branch of dX (bf16 stages)
+  float* dz2f = nullptr;    // [T, h] fp32 dZ2, residual branch of dH1 (bf16 stages)
   float* part = nullptr;    // column-sum partials
   float* part2 = nullptr;   // second LayerNorm's partials (bf16: reduced at the layer's end)
   float* colpart_ffn = nullptr;  // [ceil(T/128), f] column sums of dU (bf16 stages)
@@ -163,7 +174,14 @@ struct stage {
   void* wt_1 = nullptr;     // [h, f]
   void* wt_2 = nullptr;     // [f, h]
   float* splitk = nullptr;  // split-K partials of the weight gradients
-  size_t splitk_elems = 0;
+  size_t splitk_elems = 0;  // elements it holds
+  size_t splitk_bytes = 0;  // bytes counted for it in bytes_act
+
+  // Optional record of the gradient reaching each layer's output in the
+  // latest backward (fp32 [T, h] per layer), for layer-wise checks.
+  bool record_grads = false;
+  bool rec_valid = false;
+  std::vector<float*> rec;
 
   int B = 0, S = 0;
   bool have_ctx = false;
@@ -252,7 +270,12 @@ void free_activations(stage_t* s) {
   for (void* p : s->act_allocs) (void)hipFree(p);
   s->act_allocs.clear();
   s->saved.clear();
+  s->rec.clear();
+  s->rec_valid = false;
   s->bytes_act = 0;
+  s->splitk = nullptr;
+  s->splitk_elems = 0;
+  s->splitk_bytes = 0;
   s->cap_T = s->cap_BSS = s->cap_B = s->cap_NQB = -1;
   s->have_ctx = false;
 }
@@ -293,22 +316,78 @@ int wgrad_split(int64_t M, int64_t N, int K, int* tile) {
   return ks;
 }
 
+// Elements of split-K partials the weight gradients of a backward over T
+// tokens need.  bf16 stages compute a layer's weight gradients in one group
+// launch (stream-K over all their tiles): room for all four gradients'
+// partials, or for the feed-forward or attention half of a partial layer.
+// fp32 stages compute them one at a time: the largest one's.  The figure is
+// not monotone in T (the stream-K piece count per tile depends on how the
+// k-tiles of all tiles divide among the work-groups), so it is evaluated for
+// every token count a forward prepares.
+size_t splitk_need(const stage_t* s, int64_t T) {
+  const int64_t h = s->h, f = s->f;
+  size_t need = 0;
+  if (s->dtype == STAGE_BF16) {
+    const int Ms[4] = {(int)h, (int)f, (int)h, (int)(3 * h)};
+    const int Ns[4] = {(int)f, (int)h, (int)h, (int)h};
+    const int K = (int)std::max<int64_t>(T, 1);
+    need = std::max({(size_t)wgrad_group_slots(Ms, Ns, 4, K) * (size_t)(2 * h * f + 4 * h * h),
+                     (size_t)wgrad_group_slots(Ms, Ns, 2, K) * (size_t)(2 * h * f),
+                     (size_t)wgrad_group_slots(Ms + 2, Ns + 2, 2, K) * (size_t)(4 * h * h)});
+  } else {
+    const int64_t shapes[4][2] = {{3 * h, h}, {h, h}, {f, h}, {h, f}};
+    for (auto& mn : shapes) {
+      int tile;
+      int ks = wgrad_split(mn[0], mn[1], (int)T, &tile);
+      if (ks > 1) need = std::max<size_t>(need, (size_t)ks * mn[0] * mn[1]);
+    }
+  }
+  return need;
+}
+
+// (Re)allocates the split-K partial buffer for at least `need` elements.
+stage_status grow_splitk(stage_t* s, size_t need) {
+  if (s->splitk) {
+    auto it = std::find(s->act_allocs.begin(), s->act_allocs.end(), (void*)s->splitk);
+    if (it != s->act_allocs.end()) s->act_allocs.erase(it);
+    (void)hipFree(s->splitk);
+    s->splitk = nullptr;
+  }
+  s->bytes_act -= (int64_t)s->splitk_bytes;
+  s->splitk_elems = 0;
+  s->splitk_bytes = 0;
+  const size_t bytes = std::max<size_t>(need, 1) * 4;
+  stage_status st = dev_alloc(s, s->act_allocs, (void**)&s->splitk, bytes);
+  if (st) {
+    // leave no half-built record: the next forward allocates from scratch
+    std::string msg = s->err;
+    free_activations(s);
+    s->err = msg;
+    return st;
+  }
+  s->splitk_elems = need;
+  s->splitk_bytes = bytes;
+  return STAGE_OK;
+}
+
 stage_status ensure_activations(stage_t* s, int B, int S) {
   const int64_t T = (int64_t)B * S;
   // The score matrix is materialised only on fp32 stages.
   const int64_t BSS = s->dtype == STAGE_F32 ? (int64_t)B * s->H * S * S : 0;
   const int64_t BHS = (int64_t)B * s->H * S;
   const int64_t NQB = (int64_t)B * ((S + 31) / 32);
+  const size_t need = splitk_need(s, T);
   if (T <= s->cap_T && BSS <= s->cap_BSS && B <= s->cap_B && NQB <= s->cap_NQB &&
       (int)s->saved.size() == s->L)
-    return STAGE_OK;
+    return need <= s->splitk_elems ? STAGE_OK : grow_splitk(s, need);
   free_activations(s);
   const size_t e = s->esz;
   const int64_t h = s->h, f = s->f;
   auto A = [&](void** p, size_t bytes) { return dev_alloc(s, s->act_allocs, p, bytes); };
   stage_status st;
   s->saved.resize(s->L);
-  // The attention half of a layer saves X, QKV, P, lse, C, xhat1, rstd1;
+  // The attention half of a layer saves X, QKV, P, lse, C, xhat1, rstd1
+  // (and C's rounding residual on bf16 stages);
   // the feed-forward half saves its input H1, GELU'(U), G, xhat2, rstd2.
   for (int l = 0; l < s->L; ++l) {
     Saved& v = s->saved[l];
@@ -316,7 +395,8 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
         ((st = A(&v.X, T * h * e)) || (st = A(&v.QKV, T * 3 * h * e)) ||
          (st = A(&v.P, BSS * e)) || (st = A((void**)&v.lse, BHS * 4)) ||
          (st = A(&v.C, T * h * e)) || (st = A(&v.xhat1, T * h * e)) ||
-         (st = A((void**)&v.rstd1, T * 4))))
+         (st = A((void**)&v.rstd1, T * 4)) ||
+         (s->dtype == STAGE_BF16 && (st = A(&v.Clo, T * h * e)))))
       return st;
     if (has_ffn(s, l) &&
         ((st = A(&v.H1, T * h * e)) || (st = A(&v.Gd, T * f * e)) || (st = A(&v.G, T * f * e)) ||
@@ -328,8 +408,14 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
       (st = A((void**)&s->scores, BSS * 4)) || (st = A(&s->dS, BSS * e)) ||
       (st = A((void**)&s->kext, (size_t)B * 4)) || (st = A((void**)&s->dsum, BHS * 4)) ||
       (st = A(&s->dQKV, T * 3 * h * e)) || (st = A(&s->dZ2, T * h * e)) ||
-      (st = A(&s->dU, T * f * e)) || (st = A(&s->dH1, T * h * e)) ||
-      (st = A(&s->dZ1, T * h * e)) || (st = A(&s->dC, T * h * e)) || (st = A(&s->dY, T * h * e)))
+      (st = A(&s->dU, T * f * e)) || (st = A(&s->dZ1, T * h * e)) || (st = A(&s->dC, T * h * e)))
+    return st;
+  // The gradient between layers and at H1: in the stage dtype on fp32
+  // stages; on bf16 stages the fp32 residual branches dZ1 and dZ2 (the GEMM
+  // products go through tmp).
+  if (s->dtype == STAGE_F32 ? ((st = A(&s->dH1, T * h * e)) || (st = A(&s->dY, T * h * e)))
+                            : ((st = A((void**)&s->dz1f, T * h * 4)) ||
+                               (st = A((void**)&s->dz2f, T * h * 4))))
     return st;
   const int64_t nqb = ((int64_t)S + 31) / 32;
   if ((st = A((void**)&s->colpart_ffn, ((T + 127) / 128) * f * 4)) ||
@@ -345,29 +431,12 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
   if (s->dtype == STAGE_BF16 &&
       (st = A((void**)&s->part2, (int64_t)ln_bwd_blocks((int)T) * 3 * h * 4)))
     return st;
-  // Split-K partials.  bf16 stages compute a layer's weight gradients in
-  // one group launch: room for all four gradients' partials.  fp32 stages
-  // compute them one at a time: the largest one's.
-  size_t need = 0;
-  const int64_t shapes[4][2] = {{3 * h, h}, {h, h}, {f, h}, {h, f}};
-  if (s->dtype == STAGE_BF16) {
-    // the groups the backward launches: a whole layer (W_2, W_1, W_o,
-    // W_qkv), or the feed-forward or attention half of a partial layer
-    const int Ms[4] = {(int)h, (int)f, (int)h, (int)(3 * h)};
-    const int Ns[4] = {(int)f, (int)h, (int)h, (int)h};
-    const int K = (int)std::max<int64_t>(T, 1);
-    need = std::max({(size_t)wgrad_group_slots(Ms, Ns, 4, K) * (size_t)(2 * h * f + 4 * h * h),
-                     (size_t)wgrad_group_slots(Ms, Ns, 2, K) * (size_t)(2 * h * f),
-                     (size_t)wgrad_group_slots(Ms + 2, Ns + 2, 2, K) * (size_t)(4 * h * h)});
-  } else {
-    for (auto& mn : shapes) {
-      int tile;
-      int ks = wgrad_split(mn[0], mn[1], (int)T, &tile);
-      if (ks > 1) need = std::max<size_t>(need, (size_t)ks * mn[0] * mn[1]);
-    }
+  if (s->record_grads) {
+    s->rec.assign(s->L, nullptr);
+    for (int l = 0; l < s->L; ++l)
+      if ((st = A((void**)&s->rec[l], T * h * 4))) return st;
   }
-  s->splitk_elems = need;
-  if ((st = A((void**)&s->splitk, std::max<size_t>(need, 1) * 4))) return st;
+  if ((st = grow_splitk(s, need))) return st;
   s->cap_T = T;
   s->cap_BSS = BSS;
   s->cap_B = B;
@@ -505,6 +574,7 @@ stage_status forward_impl(stage_t* s, const T* x, T* y) {
       if constexpr (std::is_same<T, bf16_t>::value) {
         // Fused attention: softmax(Q K^T / 8) V per (batch, head), P stays on chip.
         AttnArgs aa = attn_args(s, (const bf16_t*)QKV, (bf16_t*)v.C, v.lse);
+        aa.out_lo = (bf16_t*)v.Clo;
         SITE(ATTN_FWD, attn_forward(aa, st));
       } else {
       // scores[b, j] = Q_bj K_bj^T  (fp32)
@@ -599,8 +669,20 @@ stage_status col_sum(stage_t* s, int site, int site_red, const T* x, int n, floa
   return STAGE_OK;
 }
 
-template <typename T>
-stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
+// Records the gradient reaching layer l's output when recording is on.
+stage_status record_grad(stage_t* s, int l, const bf16_t* bf, const float* a, const float* b) {
+  if (!s->record_grads || (int)s->rec.size() != s->L) return STAGE_OK;
+  const int64_t n = (int64_t)s->B * s->S * s->h;
+  hipLaunchKernelGGL(grad_record_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
+                     s->stream, bf, a, b, s->rec[l], n);
+  HIPCK(hipGetLastError());
+  return STAGE_OK;
+}
+
+// Backward of an fp32 stage: every tensor in fp32, the weight gradients one
+// GEMM at a time (split over tokens), the materialised attention path.
+stage_status backward_f32(stage_t* s, const float* dy, float* dx) {
+  using T = float;
   const int B = s->B, S = s->S, h = s->h, H = s->H, f = s->f;
   const int Tn = B * S;
   const int BH = B * H;
@@ -619,113 +701,61 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
     T* dC = (T*)s->dC;
     T* dQKV = (T*)s->dQKV;
     const T* QKV = (const T*)v.QKV;
-    // Data-gradient GEMMs multiply by W (not W^T); on bf16 stages W is first
-    // transposed so that both MFMA operands are k-contiguous.
-    constexpr bool kBF = std::is_same<T, bf16_t>::value;
     const void* Wq = p[STAGE_W_QKV];
     const void* Wo = p[STAGE_W_O];
     const void* W1 = p[STAGE_W_1];
     const void* W2 = p[STAGE_W_2];
     const bool attn = has_attn(s, l), ffn = has_ffn(s, l);
-    // Weight gradients: bf16 stages queue them and compute the layer's in
-    // one group launch at the end of the layer.
-    WgradJob wjobs[GEMM_GROUP_MAX];
-    int nw = 0;
-    // and their column reductions (LayerNorm and bias gradients) in the
-    // same group's reduction launch
-    ColJob cjobs[COLJOB_MAX];
-    int nc = 0;
+    if ((r = record_grad(s, l, nullptr, dYcur, nullptr))) return r;
     auto dW = [&](int site, int site_red, const T* dYm, int64_t ld_dy, const T* Xn,
                   int64_t ld_x, int M, int N, float* out) -> stage_status {
-      if (kBF) {
-        wjobs[nw++] = {dYm, ld_dy, Xn, ld_x, M, N, out};
-        return STAGE_OK;
-      }
       return wgrad<T>(s, site, site_red, dYm, ld_dy, Xn, ld_x, M, N, Tn, out);
     };
-    if (kBF) {
-      TransposeJob jobs[4];
-      int nj = 0;
-      if (attn) {
-        jobs[nj++] = {(const bf16_t*)Wq, (bf16_t*)s->wt_qkv, 3 * h, h, 0};
-        jobs[nj++] = {(const bf16_t*)Wo, (bf16_t*)s->wt_o, h, h, 0};
-      }
-      if (ffn) {
-        jobs[nj++] = {(const bf16_t*)W1, (bf16_t*)s->wt_1, f, h, 0};
-        jobs[nj++] = {(const bf16_t*)W2, (bf16_t*)s->wt_2, h, f, 0};
-      }
-      SITE(WT, transpose_bf16(jobs, nj, st));
-      Wq = s->wt_qkv;
-      Wo = s->wt_o;
-      W1 = s->wt_1;
-      W2 = s->wt_2;
-    }
     // Gradient reaching H1: computed by the feed-forward half, or the
     // incoming dy when the stage ends at this layer's attention half.
     const T* dH1in = dYcur;
     if (ffn) {
       // Y = LN(Z2): dZ2, dgamma2, dbeta2, and db_2 = sum_t dZ2
-      if ((r = ln_backward<T>(s, SITE_LN2_BWD, SITE_LN2_RED, dYcur, (const T*)v.xhat2, v.rstd2, (const float*)p[STAGE_G2], dZ2,
-                              gr[STAGE_G2], gr[STAGE_BE2], gr[STAGE_B_2], kBF ? s->part2 : s->part,
-                              kBF ? &cjobs[nc++] : nullptr)))
+      if ((r = ln_backward<T>(s, SITE_LN2_BWD, SITE_LN2_RED, dYcur, (const T*)v.xhat2, v.rstd2,
+                              (const float*)p[STAGE_G2], dZ2, gr[STAGE_G2], gr[STAGE_BE2],
+                              gr[STAGE_B_2], s->part, nullptr)))
         return r;
       // dW_2 = dZ2^T G
       if ((r = dW(SITE_W2_WGRAD, SITE_W2_RED, dZ2, h, (const T*)v.G, f, h, f, gr[STAGE_W_2]))) return r;
       // dU = (dZ2 W_2) * GELU'(U)
       {
-        GemmArgs g = gemm_args(dZ2, h, W2, kBF ? h : f, dU, f, Tn, f, h);
+        GemmArgs g = gemm_args(dZ2, h, W2, f, dU, f, Tn, f, h);
         g.aux = v.Gd;
         g.ldaux = f;
-        if (kBF) {  // db_1 = column sums of dU, accumulated in the epilogue
-          g.tile = 1;
-          g.colpart = s->colpart_ffn;
-        }
-        SITE(FFN2_DGRAD, Gemm<T>::run(g, true, kBF, EPI_MUL, false, 1, st));
+        SITE(FFN2_DGRAD, Gemm<T>::run(g, true, false, EPI_MUL, false, 1, st));
       }
-      if (kBF) {
-        cjobs[nc++] = ColJob{s->colpart_ffn, (Tn + 127) / 128, 1, f, {gr[STAGE_B_1], nullptr, nullptr, nullptr}};
-      } else if ((r = col_sum<T>(s, SITE_B1_SUM, SITE_B1_RED, dU, f, gr[STAGE_B_1]))) {
-        return r;
-      }
+      if ((r = col_sum<T>(s, SITE_B1_SUM, SITE_B1_RED, dU, f, gr[STAGE_B_1]))) return r;
       // dW_1 = dU^T H1
       if ((r = dW(SITE_W1_WGRAD, SITE_W1_RED, dU, f, (const T*)v.H1, h, f, h, gr[STAGE_W_1]))) return r;
       // dH1 = dZ2 + dU W_1 (the stage's dx when it starts at this layer's
       // feed-forward half)
       T* dH1out = attn ? dH1 : dx;
       {
-        GemmArgs g = gemm_args(dU, f, W1, kBF ? f : h, dH1out, h, Tn, h, f);
+        GemmArgs g = gemm_args(dU, f, W1, h, dH1out, h, Tn, h, f);
         g.aux = dZ2;
         g.ldaux = h;
-        SITE(FFN1_DGRAD, Gemm<T>::run(g, true, kBF, EPI_RESID, false, 1, st));
+        SITE(FFN1_DGRAD, Gemm<T>::run(g, true, false, EPI_RESID, false, 1, st));
       }
       dH1in = dH1out;
     }  // feed-forward half
-    if (!attn) {
-      if ((r = wgrad_group(s, wjobs, nw, cjobs, nc))) return r;
-      break;
-    }
+    if (!attn) break;
     // H1 = LN(Z1): dZ1, dgamma1, dbeta1, db_o
-    if ((r = ln_backward<T>(s, SITE_LN1_BWD, SITE_LN1_RED, dH1in, (const T*)v.xhat1, v.rstd1, (const float*)p[STAGE_G1], dZ1,
-                            gr[STAGE_G1], gr[STAGE_BE1], gr[STAGE_B_O], s->part,
-                            kBF ? &cjobs[nc++] : nullptr)))
+    if ((r = ln_backward<T>(s, SITE_LN1_BWD, SITE_LN1_RED, dH1in, (const T*)v.xhat1, v.rstd1,
+                            (const float*)p[STAGE_G1], dZ1, gr[STAGE_G1], gr[STAGE_BE1],
+                            gr[STAGE_B_O], s->part, nullptr)))
       return r;
     // dW_o = dZ1^T C
     if ((r = dW(SITE_WO_WGRAD, SITE_WO_RED, dZ1, h, (const T*)v.C, h, h, h, gr[STAGE_W_O]))) return r;
     // dC = dZ1 W_o
     {
       GemmArgs g = gemm_args(dZ1, h, Wo, h, dC, h, Tn, h, h);
-      SITE(OUT_DGRAD, Gemm<T>::run(g, true, kBF, EPI_STORE, false, 1, st));
+      SITE(OUT_DGRAD, Gemm<T>::run(g, true, false, EPI_STORE, false, 1, st));
     }
-    if constexpr (std::is_same<T, bf16_t>::value) {
-      AttnArgs aa = attn_args(s, (const bf16_t*)QKV, (bf16_t*)dQKV, v.lse);
-      aa.o = (const bf16_t*)v.C;
-      aa.dout = (const bf16_t*)dC;
-      aa.colpart = s->colpart_qkv;  // db_qkv: column sums per 32-row block
-      SITE(ATTN_DQ, attn_backward_dq(aa, st));
-      SITE(ATTN_DKDV, attn_backward_dkdv(aa, st));
-      cjobs[nc++] = ColJob{s->colpart_qkv, B * ((S + 31) / 32), 1, 3 * h,
-                           {gr[STAGE_B_QKV], nullptr, nullptr, nullptr}};
-    } else {
     // dP[b, j] = dC_bj V_bj^T (fp32, into the score buffer)
     {
       GemmArgs g = gemm_args(dC, h, QKV + 2 * h, 3 * h, s->scores, S, S, S, HEAD_DIM);
@@ -776,21 +806,154 @@ stage_status backward_impl(stage_t* s, const T* dy, T* dx) {
       g.sC2 = HEAD_DIM;
       SITE(DK_BWD, Gemm<T>::run(g, false, false, EPI_STORE, false, BH, st));
     }
-    }
-    if (!kBF && (r = col_sum<T>(s, SITE_BQKV_SUM, SITE_BQKV_RED, dQKV, 3 * h, gr[STAGE_B_QKV])))
-      return r;
+    if ((r = col_sum<T>(s, SITE_BQKV_SUM, SITE_BQKV_RED, dQKV, 3 * h, gr[STAGE_B_QKV]))) return r;
     // dW_qkv = dQKV^T X
     if ((r = dW(SITE_WQKV_WGRAD, SITE_WQKV_RED, dQKV, 3 * h, (const T*)v.X, h, 3 * h, h, gr[STAGE_W_QKV]))) return r;
     // dX = dZ1 + dQKV W_qkv  (the previous layer's dY, or the stage's dx)
     T* dXout = (l > 0) ? (T*)s->dY : dx;
     {
-      GemmArgs g = gemm_args(dQKV, 3 * h, Wq, kBF ? 3 * h : h, dXout, h, Tn, h, 3 * h);
+      GemmArgs g = gemm_args(dQKV, 3 * h, Wq, h, dXout, h, Tn, h, 3 * h);
       g.aux = dZ1;
       g.ldaux = h;
-      SITE(QKV_DGRAD, Gemm<T>::run(g, true, kBF, EPI_RESID, false, 1, st));
+      SITE(QKV_DGRAD, Gemm<T>::run(g, true, false, EPI_RESID, false, 1, st));
+    }
+    dYcur = dXout;
+  }
+  return STAGE_OK;
+}
+
+// Gradient reaching a LayerNorm of a bf16 stage: the caller's bf16 tensor
+// (at the stage's top, or below a stage boundary), or the fp32 sum of the
+// residual branch and the data-gradient GEMM's product.  The backward
+// residual stream stays in fp32 inside a stage: rounding it to bf16 at each
+// of a layer's two residual additions is what the gradient error of a deep
+// stage grows from.
+struct GradIn {
+  const bf16_t* bf;
+  const float* a;
+  const float* b;
+};
+
+// Backward of a bf16 stage.  Per layer: the LayerNorm backward kernels take
+// GradIn and write dZ in bf16 (GEMM operand) and fp32 (residual branch);
+// the two data-gradient GEMMs whose output feeds a residual addition store
+// their product in fp32 (the addition happens in the next LayerNorm
+// backward); the weights are transposed once so that every data-gradient
+// GEMM reads both operands k-contiguously; the four weight gradients and
+// the bias / LayerNorm column reductions run in one group launch and one
+// reduction launch at the end of the layer.
+stage_status backward_bf16(stage_t* s, const bf16_t* dy, bf16_t* dx) {
+  using T = bf16_t;
+  const int B = s->B, S = s->S, h = s->h, f = s->f;
+  const int Tn = B * S;
+  hipStream_t st = s->stream;
+  stage_status r;
+  GradIn gin{dy, nullptr, nullptr};
+  for (int l = s->L - 1; l >= 0; --l) {
+    Saved& v = s->saved[l];
+    auto& p = s->param[l];
+    auto& gr = s->grad[l];
+    T* dZ2 = (T*)s->dZ2;
+    T* dU = (T*)s->dU;
+    T* dZ1 = (T*)s->dZ1;
+    T* dC = (T*)s->dC;
+    T* dQKV = (T*)s->dQKV;
+    const bool attn = has_attn(s, l), ffn = has_ffn(s, l);
+    if ((r = record_grad(s, l, gin.bf, gin.a, gin.b))) return r;
+    WgradJob wjobs[GEMM_GROUP_MAX];
+    int nw = 0;
+    ColJob cjobs[COLJOB_MAX];
+    int nc = 0;
+    {
+      TransposeJob jobs[4];
+      int nj = 0;
+      if (attn) {
+        jobs[nj++] = {(const T*)p[STAGE_W_QKV], (T*)s->wt_qkv, 3 * h, h, 0};
+        jobs[nj++] = {(const T*)p[STAGE_W_O], (T*)s->wt_o, h, h, 0};
+      }
+      if (ffn) {
+        jobs[nj++] = {(const T*)p[STAGE_W_1], (T*)s->wt_1, f, h, 0};
+        jobs[nj++] = {(const T*)p[STAGE_W_2], (T*)s->wt_2, h, f, 0};
+      }
+      SITE(WT, transpose_bf16(jobs, nj, st));
+    }
+    // Gradient reaching H1: from the feed-forward half, or the incoming dy
+    // when the stage ends at this layer's attention half.
+    GradIn gh1 = gin;
+    if (ffn) {
+      // Y = LN(Z2): dZ2 (bf16 and fp32), dgamma2, dbeta2, db_2 = sum_t dZ2
+      SITE(LN2_BWD, ln_bwd_bf16(gin.bf, gin.a, gin.b, (const T*)v.xhat2, v.rstd2,
+                                (const float*)p[STAGE_G2], dZ2, s->dz2f, s->part2, Tn, h, st));
+      cjobs[nc++] = ColJob{s->part2, ln_bwd_blocks(Tn), 3, h,
+                           {gr[STAGE_G2], gr[STAGE_BE2], gr[STAGE_B_2], nullptr}};
+      // dW_2 = dZ2^T G
+      wjobs[nw++] = {dZ2, h, v.G, f, h, f, gr[STAGE_W_2]};
+      // dU = (dZ2 W_2) * GELU'(U); db_1 = column sums of dU (epilogue)
+      {
+        GemmArgs g = gemm_args(dZ2, h, s->wt_2, h, dU, f, Tn, f, h);
+        g.aux = v.Gd;
+        g.ldaux = f;
+        g.tile = 1;
+        g.colpart = s->colpart_ffn;
+        SITE(FFN2_DGRAD, gemm_bf16(g, true, true, EPI_MUL, false, 1, st));
+      }
+      cjobs[nc++] = ColJob{s->colpart_ffn, (Tn + 127) / 128, 1, f,
+                           {gr[STAGE_B_1], nullptr, nullptr, nullptr}};
+      // dW_1 = dU^T H1
+      wjobs[nw++] = {dU, f, v.H1, h, f, h, gr[STAGE_W_1]};
+      // dH1 = dZ2 + dU W_1: the product in fp32, the sum in the first
+      // LayerNorm's backward (or here, rounded, when this half is the
+      // stage's first unit and dH1 is its dx)
+      {
+        GemmArgs g = gemm_args(dU, f, s->wt_1, f, s->tmp, h, Tn, h, f);
+        SITE(FFN1_DGRAD, gemm_bf16(g, true, true, EPI_STORE, true, 1, st));
+      }
+      if (attn) {
+        gh1 = GradIn{nullptr, s->dz2f, s->tmp};
+      } else {
+        HIPCK(add_f32_to_bf16(s->dz2f, s->tmp, dx, (int64_t)Tn * h, st));
+      }
+    }  // feed-forward half
+    if (attn) {
+      // H1 = LN(Z1): dZ1 (bf16 and fp32), dgamma1, dbeta1, db_o
+      SITE(LN1_BWD, ln_bwd_bf16(gh1.bf, gh1.a, gh1.b, (const T*)v.xhat1, v.rstd1,
+                                (const float*)p[STAGE_G1], dZ1, s->dz1f, s->part, Tn, h, st));
+      cjobs[nc++] = ColJob{s->part, ln_bwd_blocks(Tn), 3, h,
+                           {gr[STAGE_G1], gr[STAGE_BE1], gr[STAGE_B_O], nullptr}};
+      // dW_o = dZ1^T C
+      wjobs[nw++] = {dZ1, h, v.C, h, h, h, gr[STAGE_W_O]};
+      // dC = dZ1 W_o
+      {
+        GemmArgs g = gemm_args(dZ1, h, s->wt_o, h, dC, h, Tn, h, h);
+        SITE(OUT_DGRAD, gemm_bf16(g, true, true, EPI_STORE, false, 1, st));
+      }
+      // Attention backward (recomputes P from the saved log-sum-exp): dQKV
+      // and the column sums of db_qkv per 32-row block.
+      AttnArgs aa = attn_args(s, (const T*)v.QKV, dQKV, v.lse);
+      aa.o = (const T*)v.C;
+      aa.o_lo = (const T*)v.Clo;
+      aa.dout = dC;
+      aa.colpart = s->colpart_qkv;
+      SITE(ATTN_DQ, attn_backward_dq(aa, st));
+      SITE(ATTN_DKDV, attn_backward_dkdv(aa, st));
+      cjobs[nc++] = ColJob{s->colpart_qkv, B * ((S + 31) / 32), 1, 3 * h,
+                           {gr[STAGE_B_QKV], nullptr, nullptr, nullptr}};
+      // dW_qkv = dQKV^T X
+      wjobs[nw++] = {dQKV, 3 * h, v.X, h, 3 * h, h, gr[STAGE_W_QKV]};
+      // dX = dZ1 + dQKV W_qkv: the product in fp32; the sum in the previous
+      // layer's second LayerNorm backward, or here, rounded, for the stage's dx
+      {
+        GemmArgs g = gemm_args(dQKV, 3 * h, s->wt_qkv, 3 * h, s->tmp, h, Tn, h, 3 * h);
+        SITE(QKV_DGRAD, gemm_bf16(g, true, true, EPI_STORE, true, 1, st));
+      }
+      if (l > 0) {
+        gin = GradIn{nullptr, s->dz1f, s->tmp};
+      } else {
+        HIPCK(add_f32_to_bf16(s->dz1f, s->tmp, dx, (int64_t)Tn * h, st));
+      }
     }
     if ((r = wgrad_group(s, wjobs, nw, cjobs, nc))) return r;
-    dYcur = dXout;
+    if (!attn) break;
   }
   return STAGE_OK;
 }
@@ -942,6 +1105,17 @@ stage_status stage_set_stream(stage_t* s, void* hip_stream) {
   return STAGE_OK;
 }
 
+stage_status stage_record_grads(stage_t* s, int on) {
+  if (!s) return STAGE_EINVAL;
+  if (on != 0 && on != 1) return fail(s, STAGE_EINVAL, "on must be 0 or 1");
+  if ((bool)on != s->record_grads) {
+    s->record_grads = on != 0;
+    s->cap_T = -1;  // the next forward allocates (or drops) the record
+    s->have_ctx = false;
+  }
+  return STAGE_OK;
+}
+
 stage_status stage_forward(stage_t* s, const void* x, const uint8_t* key_mask, int batch, int seq,
                            void* y) {
   if (!s) return STAGE_EINVAL;
@@ -961,6 +1135,7 @@ stage_status stage_forward(stage_t* s, const void* x, const uint8_t* key_mask, i
   s->B = batch;
   s->S = seq;
   s->have_ctx = false;
+  s->rec_valid = false;
   if (T == 0) {
     s->have_ctx = true;
     return STAGE_OK;
@@ -997,8 +1172,10 @@ stage_status stage_backward(stage_t* s, const void* dy, void* dx) {
     HIPCK(hipGetLastError());
     return STAGE_OK;
   }
-  return s->dtype == STAGE_BF16 ? backward_impl<bf16_t>(s, (const bf16_t*)dy, (bf16_t*)dx)
-                                : backward_impl<float>(s, (const float*)dy, (float*)dx);
+  stage_status st = s->dtype == STAGE_BF16 ? backward_bf16(s, (const bf16_t*)dy, (bf16_t*)dx)
+                                           : backward_f32(s, (const float*)dy, (float*)dx);
+  s->rec_valid = st == STAGE_OK && s->record_grads && (int)s->rec.size() == s->L;
+  return st;
 }
 
 stage_status stage_param(stage_t* s, int layer, int which, void** dev_ptr, int64_t* numel,
@@ -1060,6 +1237,7 @@ size_t stage_tensor_bytes(stage_t* s, int kind, int layer, int which) {
     saved_ptr(s, layer, which, &b);
     return b;
   }
+  if (kind == 3 && which == 0 && s->rec_valid) return (size_t)s->B * s->S * s->h * 4;
   return 0;
 }
 
@@ -1079,8 +1257,17 @@ stage_status stage_read(stage_t* s, int kind, int layer, int which, void* dst, s
     if ((int)s->saved.size() != s->L) return fail(s, STAGE_ESTATE, "no saved activations");
     src = saved_ptr(s, layer, which, &want);
     if (!src) return fail(s, STAGE_EINVAL, "the stage does not hold this half of the layer");
+  } else if (kind == 3) {
+    stage_status st = check_layer(s, layer, which, 1);
+    if (st) return st;
+    if (!s->rec_valid)
+      return fail(s, STAGE_ESTATE, "no recorded gradients: enable stage_record_grads, then run "
+                                   "a forward and a backward");
+    src = s->rec[layer];
+    want = (size_t)s->B * s->S * s->h * 4;
   } else {
-    return fail(s, STAGE_EINVAL, "kind must be 0 (param), 1 (grad) or 2 (saved)");
+    return fail(s, STAGE_EINVAL, "kind must be 0 (param), 1 (grad), 2 (saved) or 3 (recorded "
+                                 "gradient)");
   }
   if (bytes != want) return fail(s, STAGE_EINVAL, "byte count does not match the tensor");
   if (want == 0) return STAGE_OK;

@@ -117,7 +117,13 @@ def test_bitwise_determinism(dtype):
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_partition_invariance(dtype):
     """Layers [0,3) as one stage == stage [0,1) then stage [1,3), chained
-    through y -> x forward and dx -> dy backward (bitwise)."""
+    through y -> x forward and dx -> dy backward.  Bitwise on fp32 stages and
+    in the bf16 forward pass (the tensor between layers is the bf16 layer
+    output either way).  In the bf16 backward pass the gradient crossing
+    the boundary is the bf16 dx of the upper stage, while inside one stage
+    it stays fp32: there the two agree to the rounding of that one tensor
+    (relative L2 <= 1e-2, the bf16 gradient tolerance, on dx and every
+    gradient)."""
     import torch
     cfg = synth.StageConfig("part", 3, 128, 2, 256, 2, 32, 8, 32, dtype, 9)
     _say(f"case partition {dtype}")
@@ -137,11 +143,20 @@ def test_partition_invariance(dtype):
     d0 = first.backward(d1)
     torch.cuda.synchronize()
     assert torch.equal(y, y2)
-    assert torch.equal(dx, d0)
-    for w in range(12):
-        assert torch.equal(whole.grad(0, w), first.grad(0, w))
-        assert torch.equal(whole.grad(1, w), second.grad(0, w))
-        assert torch.equal(whole.grad(2, w), second.grad(1, w))
+    # (whole stage, chained stages): dx, then layer 0's 12 gradients (in
+    # `first`), then layers 1 and 2 (layers 0 and 1 of `second`)
+    pairs = [(dx, d0)] + [(whole.grad(l, w), first.grad(0, w) if l == 0 else second.grad(l - 1, w))
+                          for l in range(3) for w in range(12)]
+    for k, (a, b) in enumerate(pairs):
+        if dtype == "f32" or k >= 1 + 12:  # layers above the boundary see the same inputs
+            assert torch.equal(a, b), k
+        else:
+            a, b = a.float(), b.float()
+            e = float((a - b).norm() / b.norm().clamp_min(1e-30))
+            if k == 1 + 1:  # the key-bias gradient is ~0: its norm against the query's
+                e = float((a[128:256] - b[128:256]).norm() / b[:128].norm())
+            print(f"  chained vs whole, pair {k}: rel l2 {e:.2e}", flush=True)
+            assert e <= 1e-2, (k, e)
     for s in (whole, first, second):
         s.close()
 
@@ -177,3 +192,50 @@ def test_mfma_peak_measurement():
     assert 0.5 < ghz < 2.6
     assert 200.0 < tf <= 2516.6 * 1.01
     assert tf <= 2516.6 * ghz / 2.4 * 1.05
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_recorded_gradients(dtype):
+    """stage_record_grads: after a backward, stage_read kind 3 gives the
+    gradient that reached each layer's output: dy at the top layer, and at
+    layer 0 what the upper two layers hand down, i.e. the dx of a stage of
+    those two layers (bitwise on fp32; on bf16 that dx is the recorded fp32
+    value rounded to bf16).  Without recording, or after a new forward,
+    kind 3 is a state error."""
+    import torch
+    import paper_2202_11836_amd as P
+    cfg = synth.StageConfig("rec", 3, 128, 2, 256, 2, 32, 8, 32, dtype, 5)
+    _say(f"case recorded gradients {dtype}")
+    inp = synth.make_inputs(cfg)
+    params = synth.make_params(cfg, perturb=True)
+    whole = make_stage(cfg, params)
+    upper = make_stage(cfg.with_(L=2), params[1:])
+    x = to_torch(inp["x"], dtype)
+    mask = torch.from_numpy(inp["mask"]).cuda()
+    dy = to_torch(inp["dy"], dtype)
+    T = cfg.batch * cfg.seq
+    whole.forward(x, mask)
+    whole.backward(dy)
+    with pytest.raises(P.StageError) as e:
+        whole.recorded_grad(0, T)
+    assert e.value.status == P.binding.STAGE_ESTATE
+    whole.record_grads(True)
+    y = whole.forward(x, mask)
+    dx = whole.backward(dy)
+    y0 = whole.saved(1, 0, T).view_as(x)  # layer 0's output = layer 1's input
+    upper.forward(y0, mask)
+    d1 = upper.backward(dy)
+    torch.cuda.synchronize()
+    assert torch.equal(whole.recorded_grad(2, T), dy.reshape(T, -1).float())
+    r0 = whole.recorded_grad(0, T)
+    if dtype == "f32":
+        assert torch.equal(r0, d1.reshape(T, -1))
+    else:
+        assert torch.equal(r0.to(torch.bfloat16), d1.reshape(T, -1))
+    assert P.stage_tensor_bytes(whole.handle, 3, 0, 0) == T * cfg.hidden * 4
+    whole.forward(x, mask)
+    with pytest.raises(P.StageError) as e:
+        whole.recorded_grad(0, T)
+    assert e.value.status == P.binding.STAGE_ESTATE
+    for s in (whole, upper):
+        s.close()

@@ -4,16 +4,22 @@ Tolerances:
   * fp32 stages: per tensor ||gpu - ref||_inf / ||ref||_inf <= 1e-4 for y,
     dx, every parameter gradient and the saved activations.
   * bf16 stages (bf16 storage, fp32 accumulation): max |gpu - ref| <= 2e-2
-    on the LayerNorm outputs (H1 and Y) of every layer, or one bf16 ulp of
-    the reference value where that is larger (bf16 cannot represent values
-    of magnitude >= 4 closer than 0.0156, >= 8 closer than 0.031), the oracle
-    running each layer from the GPU's own bf16 input of that layer
-    (layer-wise: the rounding of a layer's output is inherited by the next
-    layer and is not a kernel error); and ||gpu - ref||_2 / ||ref||_2 <= 1e-2
-    end to end for y, dx and every parameter gradient tensor.
-    On fp32 stages the key bias gradient, analytically zero (softmax is
-    invariant to a per-row shift), is checked against the query bias
-    gradient's norm.
+    on the LayerNorm outputs (H1 and Y) of every layer, the oracle running
+    each layer from the GPU's own bf16 input of that layer (layer-wise: the
+    rounding of a layer's output is inherited by the next layer and is not a
+    kernel error).  Where half a bf16 ulp of the reference value plus a
+    compute allowance of 2^-10 |ref| exceeds 2e-2 (|ref| >= 4), that is the
+    bound instead: a bf16 output is the fp32 result rounded to 8 significant
+    bits, so an output of magnitude in [4, 8) is off by up to 0.0156 from
+    the exact value by rounding alone, one in [8, 16) by up to 0.031.  Each
+    tensor reports whether it also meets the literal 2e-2.  Gradients:
+    ||gpu - ref||_2 / ||ref||_2 <= 1e-2 end to end for y, dx and every
+    parameter gradient tensor, with the key-bias block of b_qkv excluded.
+  * The key-bias gradient is analytically zero (section II-C, Eq. (1): the
+    row softmax is invariant to adding a constant to every score of a row,
+    and the key bias adds q . b_k to all scores of query q's row), so it is
+    checked as ||db_k||_2 <= tol * ||db_q||_2 on every stage, tol = 1e-4 on
+    fp32 stages and 1e-2 on bf16 stages.
 """
 import numpy as np
 import pytest
@@ -26,6 +32,7 @@ pytestmark = pytest.mark.gpu
 F32_TOL = 1e-4
 BF16_LN_ABS = 2e-2
 BF16_GRAD_L2 = 1e-2
+BF16_DBK_REL = 1e-2  # ||db_k|| / ||db_q|| on bf16 stages
 
 
 def _say(msg):
@@ -64,10 +71,17 @@ def check_f32(cfg, got, ref, saved_gpu=None):
                 assert e <= F32_TOL, (l, key, e)
 
 
+def ln_bound(r: np.ndarray) -> np.ndarray:
+    """Per-element bound on a bf16 LayerNorm output: 2e-2, or half a bf16
+    ulp of the reference plus 2^-10 |ref| where that is larger."""
+    return np.maximum(BF16_LN_ABS, 0.5 * bf16_ulp(r) + np.abs(r) * 2.0 ** -10)
+
+
 def check_bf16_layerwise(cfg, inp, params, got, seqs=None):
     """Each layer recomputed by the oracle from the GPU's own (bf16) input of
     that layer: max |gpu - ref| on its two LayerNorm outputs H1 and Y.
-    seqs: optional sequence indices to check (others skipped)."""
+    seqs: optional sequence indices to check (others skipped).  Returns the
+    worst error as a multiple of 2e-2 on the ln_bound scale (<= 2e-2 passes)."""
     import oracle
     B, S, h = cfg.batch, cfg.seq, cfg.hidden
     sel = np.arange(B) if seqs is None else np.asarray(seqs)
@@ -79,15 +93,20 @@ def check_bf16_layerwise(cfg, inp, params, got, seqs=None):
         y_ref, sv = oracle.layer_forward(X[l], mask, params[l], cfg.heads)
         y_gpu = X[l + 1] if l + 1 < cfg.L else got["y"][sel]
         for name, g, r in (("H1", H1[l].reshape(-1, h), sv["H1"]), ("Y", y_gpu, y_ref)):
-            g, r = g.reshape(-1), r.reshape(-1)
-            err = np.abs(g - r)
-            # normalised: error over max(2e-2, one bf16 ulp of the reference)
-            norm = err / np.maximum(BF16_LN_ABS, bf16_ulp(r))
-            i = int(np.argmax(norm))
-            _say(f"  layer {l} {name}: max abs {err.max():.3e}; worst vs bound {norm[i]:.3f} "
-                 f"(err {err[i]:.3e} at ref {r[i]:+.3f})")
-            worst = max(worst, float(norm[i]))
+            worst = max(worst, report_ln(f"layer {l} {name}", g.reshape(-1), r.reshape(-1)))
     return worst * BF16_LN_ABS
+
+
+def report_ln(label, g, r) -> float:
+    """Prints the LayerNorm-output check of one tensor; returns its worst
+    error over ln_bound (<= 1 passes)."""
+    err = np.abs(g - r)
+    norm = err / ln_bound(r)
+    i = int(np.argmax(norm))
+    literal = "meets" if err.max() <= BF16_LN_ABS else "exceeds (passes on the half-ulp bound)"
+    _say(f"  {label}: max abs {err.max():.3e} {literal} 2e-2; worst vs bound {norm[i]:.3f} "
+         f"(err {err[i]:.3e} at ref {r[i]:+.3f})")
+    return float(norm[i])
 
 
 def bf16_ulp(r: np.ndarray) -> np.ndarray:
@@ -96,8 +115,10 @@ def bf16_ulp(r: np.ndarray) -> np.ndarray:
     return np.exp2(e - 7)
 
 
-def check_bf16(cfg, got, ref, grad_tol=BF16_GRAD_L2, rows=None):
-    """End to end: relative L2 of y, dx and every parameter gradient.
+def check_bf16(cfg, got, ref, rows=None):
+    """End to end: relative L2 of y, dx and every parameter gradient (the
+    key-bias block of b_qkv excluded), plus the key-bias pin: the ratio
+    ||db_k|| / ||db_q|| under the key (layer, "db_k/db_q").
     rows: optional boolean [B] selecting the sequences y/dx are compared on."""
     h = cfg.hidden
     y_g, y_r = got["y"], ref["y"]
@@ -109,16 +130,26 @@ def check_bf16(cfg, got, ref, grad_tol=BF16_GRAD_L2, rows=None):
     e = rel_l2(dx_g, dx_r)
     _say(f"  dx rel l2 {e:.3e}")
     worst = {("dx",): e, ("y",): e_y}
+    kq_worst = 0.0
     for l in range(cfg.L):
         for name in synth.PARAM_NAMES:
-            worst[(l, name)] = rel_l2(got["grads"][l][name], ref["grads"][l][name])
+            g, r = got["grads"][l][name], ref["grads"][l][name]
+            if name == "b_qkv":
+                kq = float(np.linalg.norm(g[h:2 * h]) / max(np.linalg.norm(r[:h]), 1e-30))
+                kq_worst = max(kq_worst, kq)
+                worst[(l, "db_k/db_q")] = kq
+                g = np.concatenate([g[:h], g[2 * h:]])
+                r = np.concatenate([r[:h], r[2 * h:]])
+            worst[(l, name)] = rel_l2(g, r)
+    _say(f"  key-bias pin: max ||db_k|| / ||db_q|| = {kq_worst:.3e} (bound {BF16_DBK_REL:g})")
     for k in sorted(worst, key=worst.get, reverse=True)[:4]:
         _say(f"  rel l2 {worst[k]:.3e} at {k}")
     return worst
 
 
 def assert_bf16(layerwise_worst, e2e):
-    bad = {k: e for k, e in e2e.items() if not e <= BF16_GRAD_L2}
+    bad = {k: e for k, e in e2e.items()
+           if not e <= (BF16_DBK_REL if k[-1] == "db_k/db_q" else BF16_GRAD_L2)}
     assert layerwise_worst <= BF16_LN_ABS and not bad, (layerwise_worst, bad)
 
 
@@ -234,3 +265,37 @@ def test_bf16_bert_base_8_uneven_sequence_subset():
     sub = {"x": inp["x"][sel], "mask": inp["mask"][sel], "dy": dy[sel]}
     ref = run_oracle(cfg.with_(batch=int(sel.sum())), sub, params)
     assert_bf16(lw, check_bf16(cfg, got, ref, rows=sel))
+
+
+def test_bf16_smaller_batches_after_the_full_batch():
+    """One BERT-large-shaped layer run on B32 x S512 and then, on the same
+    stage, on smaller batches.  The weight-gradient stream-K schedule of a
+    smaller token count can need more split-K partials than the full batch
+    (T = 384 needs 201 MB against 101 MB at T = 16384): every call must still
+    match the oracle.  The full batch is checked on sequences {0, 31} (dy
+    zero elsewhere), the smaller ones whole."""
+    from _parity import make_stage
+    base = synth.CONFIGS["bert_large_4"].with_(L=1)
+    params = synth.make_params(base, perturb=True)
+    st = make_stage(base, params)
+    try:
+        for batch, seq in ((32, 512), (1, 384), (1, 192), (3, 96)):
+            cfg = base.with_(batch=batch, seq=seq, len_lo=seq // 2, len_hi=seq)
+            _say(f"case bf16 B{batch} x S{seq} after the full batch")
+            inp = synth.make_inputs(cfg, seed=batch * 1000 + seq)
+            if batch == 32:
+                sel = np.zeros(batch, bool)
+                sel[[0, batch - 1]] = True
+                dy = inp["dy"].copy()
+                dy[~sel] = 0.0
+                got = run_gpu(cfg, inp, params, dy=dy, stage=st, saved=(0, 3))
+                lw = check_bf16_layerwise(cfg, inp, params, got, seqs=np.flatnonzero(sel))
+                sub = {"x": inp["x"][sel], "mask": inp["mask"][sel], "dy": dy[sel]}
+                ref = run_oracle(cfg.with_(batch=2), sub, params)
+                assert_bf16(lw, check_bf16(cfg, got, ref, rows=sel))
+            else:
+                got = run_gpu(cfg, inp, params, stage=st, saved=(0, 3))
+                lw = check_bf16_layerwise(cfg, inp, params, got)
+                assert_bf16(lw, check_bf16(cfg, got, run_oracle(cfg, inp, params)))
+    finally:
+        st.close()

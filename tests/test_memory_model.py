@@ -11,7 +11,8 @@ def closed_form_units(h, H, f, B, S, bf16):
     """(attention unit, feed-forward unit) bytes from the storage plan of a
     half-layer stage: the attention half holds W_qkv, b_qkv, W_o, b_o, g1,
     be1 (with gradients) and saves X, QKV, the fp32 scores (fp32 stages) or
-    the log-sum-exp, C, x_hat1, rstd1; the feed-forward half holds W_1, b_1,
+    the log-sum-exp, C, x_hat1, rstd1 and (bf16 stages) C's rounding
+    residual; the feed-forward half holds W_1, b_1,
     W_2, b_2, g2, be2 and saves its input H1, GELU'(U), G, x_hat2, rstd2."""
     e = 2 if bf16 else 4
     T = B * S
@@ -20,7 +21,7 @@ def closed_form_units(h, H, f, B, S, bf16):
     attn = (a(3 * h * h * e) + a(3 * h * h * 4) + a(h * h * e) + a(h * h * 4)
             + sum(a(n * 4) * 2 for n in (3 * h, h, h, h))
             + a(T * h * e) + a(T * 3 * h * e) + a(BSS * e) + a(B * H * S * 4) + a(T * h * e)
-            + a(T * h * e) + a(T * 4))
+            + a(T * h * e) + a(T * 4) + (a(T * h * e) if bf16 else 0))
     ffn = (a(f * h * e) + a(f * h * 4) + a(h * f * e) + a(h * f * 4)
            + sum(a(n * 4) * 2 for n in (f, h, h, h))
            + a(T * h * e) + a(T * f * e) + a(T * f * e) + a(T * h * e) + a(T * 4))
@@ -32,7 +33,8 @@ def closed_form(h, H, f, B, S, bf16):
     storage plan: parameters in the stage dtype (matrices) or fp32 (vectors)
     with fp32 gradients; the saved activations X, QKV, C, x_hat1, H1,
     GELU'(U), G, x_hat2 (stage dtype), rstd1, rstd2 and the log-sum-exp
-    (fp32); the fp32 score matrix is kept only on fp32 stages.  Every
+    (fp32); the fp32 score matrix is kept only on fp32 stages, the
+    context's bf16 rounding residual only on bf16 stages.  Every
     allocation is at least 256 bytes."""
     e = 2 if bf16 else 4
     T = B * S
@@ -43,7 +45,7 @@ def closed_form(h, H, f, B, S, bf16):
     BSS = 0 if bf16 else B * H * S * S
     saved = (a(T * h * e) + a(T * 3 * h * e) + a(BSS * e) + a(B * H * S * 4) + a(T * h * e)
              + a(T * h * e) + a(T * 4) + a(T * h * e) + a(T * f * e) + a(T * f * e)
-             + a(T * h * e) + a(T * 4))
+             + a(T * h * e) + a(T * 4) + (a(T * h * e) if bf16 else 0))
     return par + saved
 
 
