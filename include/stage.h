@@ -163,6 +163,26 @@ stage_status stage_forward(stage_t* s, const void* x, const uint8_t* key_mask, i
 stage_status stage_backward(stage_t* s, const void* dy, void* dx);
 
 /*
+ * For callers that cannot allocate device memory during the call (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * stage_backward with the same kernels and results, bitwise, whose
+ * weight-gradient split-K partials and bias / LayerNorm column partial sums
+ * live in a static device array of 256 MiB (one per device, held from the
+ * library's first use on that device until the process ends) instead of
+ * buffers of the stage.  It calls no allocator (no hipMalloc / hipFree, no
+ * HIP events: stage tracing does not see its launches).  Every call on a
+ * device shares that device's array and leaves its contents behind: calls
+ * that overlap on one device (several stages on concurrent streams) race
+ * and must be serialised by the caller.  EINVAL (context kept) when the
+ * batch needs more partial results than the array holds: the split-K
+ * partials grow with h f (about 201 MB at most for h = 1024, f = 4096, and
+ * for h = 2048, f = 8192), the column partial sums with the token count
+ * (about 2.6 KB per token at h = 2048); e.g. h = 2048, f = 8192 at 32768
+ * tokens does not fit.  Otherwise as stage_backward.
+ */
+stage_status stage_backward_noalloc(stage_t* s, const void* dy, void* dx);
+
+/*
  * Device memory.  stage_device_bytes: bytes the library holds for s
  * (parameters, gradients, the saved-activation record and the workspace, as
  * requested from hipMalloc).  stage_memory_model: the same figure predicted

@@ -33,6 +33,7 @@ EXPORTED = ("alloc_coarse", "alloc_fine", "alloc_workloads", "stage_init", "stag
             "stage_trace_site", "stage_trace_mask", "stage_trace_read", "stage_site_count",
             "stage_site_name", "stage_device_bytes", "stage_memory_model",
             "stage_memory_model_units", "stage_mfma_peak", "stage_record_grads",
+            "stage_backward_noalloc",
             "stage_last_error", "stage_destroy")
 
 _lib = None
@@ -74,6 +75,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.stage_forward.restype = i32
     lib.stage_backward.argtypes = [vp, vp, vp]
     lib.stage_backward.restype = i32
+    lib.stage_backward_noalloc.argtypes = [vp, vp, vp]
+    lib.stage_backward_noalloc.restype = i32
     lib.stage_param.argtypes = [vp, i32, i32, ctypes.POINTER(vp), ctypes.POINTER(i64), ctypes.POINTER(i32)]
     lib.stage_param.restype = i32
     lib.stage_grad.argtypes = [vp, i32, i32, ctypes.POINTER(vp), ctypes.POINTER(i64)]
@@ -177,6 +180,10 @@ def stage_forward(handle, x, key_mask, batch: int, seq: int, y) -> None:
 
 def stage_backward(handle, dy, dx) -> None:
     _check(handle, load_library().stage_backward(handle, _ptr(dy), _ptr(dx)))
+
+
+def stage_backward_noalloc(handle, dy, dx) -> None:
+    _check(handle, load_library().stage_backward_noalloc(handle, _ptr(dy), _ptr(dx)))
 
 
 def stage_param(handle, layer: int, which: int):
@@ -321,6 +328,16 @@ class Stage:
         self._sync_stream()
         stage_backward(self.handle, dy, dx)
         return dx
+
+    def backward_noalloc(self, dy, out):
+        """Backward with the partial results in the library's static
+        scratch (stage_backward_noalloc); out must be given."""
+        import torch
+        assert dy.dtype == self.torch_dtype and dy.is_cuda and dy.is_contiguous()
+        assert out is not None and out.dtype == dy.dtype and out.shape == dy.shape
+        self._sync_stream()
+        stage_backward_noalloc(self.handle, dy, out)
+        return out
 
     def _param_shape(self, which: int):
         h, f = self.hidden, self.ffn

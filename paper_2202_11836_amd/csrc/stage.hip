@@ -9,6 +9,7 @@
 #include <array>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <type_traits>
@@ -122,6 +123,14 @@ struct Saved {
 
 }  // namespace
 
+// Static scratch of stage_backward_noalloc: the weight-gradient split-K
+// partials and the bias / LayerNorm column partial sums of a backward pass,
+// in a file-scope device array (one copy per device, held until the process
+// ends).  Host code never uses its name as an address: the per-device
+// address comes from hipGetSymbolAddress (resolve_scratch).
+constexpr size_t NOALLOC_SCRATCH_BYTES = (size_t)256 << 20;
+static __device__ __align__(256) float scratch[NOALLOC_SCRATCH_BYTES / sizeof(float)];
+
 struct stage {
   int L = 0, h = 0, H = 0, f = 0;
   // Allocation units (two per encoder layer): unit 2j is the attention half
@@ -183,6 +192,9 @@ struct stage {
   bool rec_valid = false;
   std::vector<float*> rec;
 
+  int device = 0;          // device current at stage_init
+  bool no_alloc = false;   // inside stage_backward_noalloc: no event creation
+
   int B = 0, S = 0;
   bool have_ctx = false;
   std::string err;
@@ -197,6 +209,35 @@ namespace {
 
 // Message of the last failed stage_init on this thread (no handle exists).
 thread_local std::string g_init_err;
+
+// Per-device address of `scratch`, resolved once per device with that device
+// current (at stage_init).
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[MAX_DEVICES] = {};
+
+// Resolves (once) the address of `scratch` on the current device.
+hipError_t resolve_scratch(int* device_out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= MAX_DEVICES) return hipErrorInvalidDevice;
+  if (device_out) *device_out = dev;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev]) return hipSuccess;
+  void* ptr = nullptr;
+  e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+  if (e != hipSuccess) return e;
+  g_scratch_ptr[dev] = (float*)ptr;
+  return hipSuccess;
+}
+
+float* scratch_of(int dev) {
+  if (dev < 0 || dev >= MAX_DEVICES) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  return g_scratch_ptr[dev];
+}
 
 // Which halves of local layer l the stage holds.
 bool has_attn(const stage_t* s, int l) { return !(l == 0 && s->ffn_first); }
@@ -220,7 +261,7 @@ stage_status fail(stage_t* s, stage_status st, const std::string& msg) {
 // Records a start event before a traced site's launch; returns the pool
 // index of the event pair, or -1 when the site is not traced.
 int trace_begin(stage_t* s, int site) {
-  if (!((s->trace_mask >> site) & 1)) return -1;
+  if (!((s->trace_mask >> site) & 1) || s->no_alloc) return -1;
   while (s->events.size() < s->events_used + 2) {
     hipEvent_t e;
     if (hipEventCreate(&e) != hipSuccess) return -1;
@@ -1089,6 +1130,11 @@ stage_status stage_init_units(int first_unit, int n_units, int hidden, int heads
   set_units(s, first_unit, n_units, hidden, heads, ffn, dtype);
   s->stream = (hipStream_t)hip_stream;
   stage_status st = build_params(s, seed);
+  if (!st) {
+    const hipError_t e = resolve_scratch(&s->device);
+    if (e != hipSuccess)
+      st = fail(s, STAGE_EHIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+  }
   if (st) {
     g_init_err = s->err;
     for (void* p : s->allocs) (void)hipFree(p);
@@ -1175,6 +1221,59 @@ stage_status stage_backward(stage_t* s, const void* dy, void* dx) {
   stage_status st = s->dtype == STAGE_BF16 ? backward_bf16(s, (const bf16_t*)dy, (bf16_t*)dx)
                                            : backward_f32(s, (const float*)dy, (float*)dx);
   s->rec_valid = st == STAGE_OK && s->record_grads && (int)s->rec.size() == s->L;
+  return st;
+}
+
+stage_status stage_backward_noalloc(stage_t* s, const void* dy, void* dx) {
+  if (!s) return STAGE_EINVAL;
+  s->err.clear();
+  if (!s->have_ctx) return fail(s, STAGE_ESTATE, "stage_backward needs a preceding stage_forward");
+  float* base = scratch_of(s->device);
+  if (!base) return fail(s, STAGE_ESTATE, "static scratch not resolved for the stage's device");
+  // The backward's partial buffers, laid out in the scratch (256-byte
+  // aligned slices).  Every element the kernels read is written earlier in
+  // the same call, so nothing needs clearing.
+  const int64_t T = (int64_t)s->B * s->S;
+  const int64_t h = s->h, f = s->f;
+  const int64_t nlnb = ln_bwd_blocks((int)T);
+  const size_t need_splitk = splitk_need(s, T);
+  const size_t n_part = (size_t)std::max<int64_t>(nlnb * 3 * h, (int64_t)COL_PARTS * std::max<int64_t>(3 * h, f));
+  const size_t n_part2 = (size_t)(nlnb * 3 * h);
+  const size_t n_cffn = (size_t)(((T + 127) / 128) * f);
+  const size_t n_cqkv = (size_t)((int64_t)s->B * ((s->S + 31) / 32) * 3 * h);
+  size_t off = 0;
+  auto take = [&](size_t elems) {
+    float* p = base + off;
+    off += (std::max<size_t>(elems, 1) + 63) / 64 * 64;
+    return p;
+  };
+  float* sk = take(need_splitk);
+  float* pt = take(n_part);
+  float* pt2 = take(n_part2);
+  float* cf = take(n_cffn);
+  float* cq = take(n_cqkv);
+  if (off * sizeof(float) > NOALLOC_SCRATCH_BYTES)
+    return fail(s, STAGE_EINVAL,
+                "stage_backward_noalloc: this batch needs " + std::to_string(off * sizeof(float)) +
+                    " bytes of partial results; the static scratch holds " +
+                    std::to_string(NOALLOC_SCRATCH_BYTES) + " (use stage_backward)");
+  float* const keep[5] = {s->splitk, s->part, s->part2, s->colpart_ffn, s->colpart_qkv};
+  const size_t keep_elems = s->splitk_elems;
+  s->splitk = sk;
+  s->splitk_elems = need_splitk;
+  s->part = pt;
+  s->part2 = pt2;
+  s->colpart_ffn = cf;
+  s->colpart_qkv = cq;
+  s->no_alloc = true;
+  const stage_status st = stage_backward(s, dy, dx);
+  s->no_alloc = false;
+  s->splitk = keep[0];
+  s->splitk_elems = keep_elems;
+  s->part = keep[1];
+  s->part2 = keep[2];
+  s->colpart_ffn = keep[3];
+  s->colpart_qkv = keep[4];
   return st;
 }
 
