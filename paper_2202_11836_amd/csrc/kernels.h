@@ -127,13 +127,14 @@ hipError_t ln_bwd(const T* dy, const T* xhat, const float* rstd, const float* ga
                   float* part, int rows, int h, hipStream_t st);
 
 // bf16 stages: the same with dy either one bf16 tensor (dya = dyb = null)
-// or the fp32 sum dya + dyb (dy = null); dz in bf16 and, when dz32 is not
-// null, in fp32 as well.  Partials as ln_bwd.
-hipError_t ln_bwd_bf16(const bf16_t* dy, const float* dya, const float* dyb, const bf16_t* xhat,
+// or the sum dya + dyb of an fp32 and a bf16 tensor, in fp32 (dy = null);
+// dz in bf16 and, when dz32 is not null, in fp32 as well.  Partials as
+// ln_bwd.
+hipError_t ln_bwd_bf16(const bf16_t* dy, const float* dya, const bf16_t* dyb, const bf16_t* xhat,
                        const float* rstd, const float* gamma, bf16_t* dz, float* dz32,
                        float* part, int rows, int h, hipStream_t st);
-// out = bf16(a + b), n elements (a multiple of 8).
-hipError_t add_f32_to_bf16(const float* a, const float* b, bf16_t* out, int64_t n,
+// out = bf16(a + b), a fp32, b bf16, n elements (a multiple of 8).
+hipError_t add_f32_to_bf16(const float* a, const bf16_t* b, bf16_t* out, int64_t n,
                            hipStream_t st);
 
 // dst[c][r] = src[r][c] for a bf16 [R][C] matrix.

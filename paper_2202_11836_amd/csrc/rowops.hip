@@ -237,14 +237,15 @@ __device__ __forceinline__ float bf_at(const u32x4_t& r, int k) {
 }
 
 // The incoming gradient dy is either one bf16 tensor or, when SUM32, the
-// sum of two fp32 tensors dya + dyb (the backward residual stream of a bf16
-// stage: the fp32 gradient of the residual branch plus the fp32 product of
-// the data-gradient GEMM, so that the stream is never rounded to bf16).
+// sum dya + dyb of an fp32 and a bf16 tensor (the backward residual stream
+// of a bf16 stage: the fp32 gradient of the residual branch plus the bf16
+// product of the data-gradient GEMM, so that the stream itself is never
+// rounded to bf16).
 // dz goes out in bf16 (the operand of the following GEMMs) and, when dz32
 // is not null, in fp32 as well (the residual branch of the next addition).
 template <int NC, bool SUM32>
 __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(
-    const bf16_t* __restrict__ dy, const float* __restrict__ dya, const float* __restrict__ dyb,
+    const bf16_t* __restrict__ dy, const float* __restrict__ dya, const bf16_t* __restrict__ dyb,
     const bf16_t* __restrict__ xhat, const float* __restrict__ rstd,
     const float* __restrict__ gamma, bf16_t* __restrict__ dz, float* __restrict__ dz32,
     float* __restrict__ part, int rows, int h, int rpb) {
@@ -265,9 +266,10 @@ __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(
   const int r1 = min(rows, r0 + rpb);
   const float inv_h = 1.0f / (float)h;
   for (int row0 = r0 + wave; row0 < r1; row0 += 8) {
-    // SUM32: dy as fp32 (two 16-byte halves of each addend); else packed bf16
+    // SUM32: the fp32 addend as two 16-byte halves and the bf16 addend
+    // packed; else dy packed bf16
     u32x4_t dr[2][NC], xr[2][NC];
-    f32x4_t fa[2][NC][2], fb[2][NC][2];
+    f32x4_t fa[2][NC][2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int row = row0 + 4 * u;
@@ -279,18 +281,14 @@ __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(
           if constexpr (SUM32) {
             fa[u][i][0] = *(const f32x4_t*)(dya + base + 8 * c);
             fa[u][i][1] = *(const f32x4_t*)(dya + base + 8 * c + 4);
-            fb[u][i][0] = *(const f32x4_t*)(dyb + base + 8 * c);
-            fb[u][i][1] = *(const f32x4_t*)(dyb + base + 8 * c + 4);
+            dr[u][i] = *(const u32x4_t*)(dyb + base + 8 * c);
           } else {
             dr[u][i] = *(const u32x4_t*)(dy + base + 8 * c);
           }
           xr[u][i] = *(const u32x4_t*)(xhat + base + 8 * c);
         } else {
-          if constexpr (SUM32) {
-            fa[u][i][0] = fa[u][i][1] = fb[u][i][0] = fb[u][i][1] = f32x4_t{0, 0, 0, 0};
-          } else {
-            dr[u][i] = u32x4_t{0, 0, 0, 0};
-          }
+          if constexpr (SUM32) fa[u][i][0] = fa[u][i][1] = f32x4_t{0, 0, 0, 0};
+          dr[u][i] = u32x4_t{0, 0, 0, 0};
           xr[u][i] = u32x4_t{0, 0, 0, 0};
         }
       }
@@ -298,7 +296,7 @@ __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(
     // the incoming gradient at (u, i, k)
     auto dyv = [&](int u, int i, int k) -> float {
       if constexpr (SUM32)
-        return fa[u][i][k >> 2][k & 3] + fb[u][i][k >> 2][k & 3];
+        return fa[u][i][k >> 2][k & 3] + bf_at(dr[u][i], k);
       else
         return bf_at(dr[u][i], k);
     };
@@ -375,9 +373,10 @@ __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(
     P[e] = ((red[e] + red[3 * h + e]) + red[6 * h + e]) + red[9 * h + e];
 }
 
-// out = a + b rounded to bf16, 8 elements per thread (n % 8 == 0).
+// out = a + b rounded to bf16 (a fp32, b bf16), 8 elements per thread
+// (n % 8 == 0).
 __global__ __launch_bounds__(256) void add_f32_to_bf16_kernel(const float* __restrict__ a,
-                                                              const float* __restrict__ b,
+                                                              const bf16_t* __restrict__ b,
                                                               bf16_t* __restrict__ out, int64_t n8) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= n8) return;
@@ -548,7 +547,7 @@ hipError_t add_ln_fwd(const TA* a, const float* bias, const TR* resid, const flo
 
 int ln_bwd_blocks(int rows) { return (rows + LN_BWD_RPB - 1) / LN_BWD_RPB; }
 
-hipError_t ln_bwd_bf16(const bf16_t* dy, const float* dya, const float* dyb, const bf16_t* xhat,
+hipError_t ln_bwd_bf16(const bf16_t* dy, const float* dya, const bf16_t* dyb, const bf16_t* xhat,
                        const float* rstd, const float* gamma, bf16_t* dz, float* dz32,
                        float* part, int rows, int h, hipStream_t st) {
   if (h % 64 != 0 || h > 2048) return hipErrorInvalidValue;
@@ -580,7 +579,7 @@ hipError_t ln_bwd_bf16(const bf16_t* dy, const float* dya, const float* dyb, con
   return hipGetLastError();
 }
 
-hipError_t add_f32_to_bf16(const float* a, const float* b, bf16_t* out, int64_t n,
+hipError_t add_f32_to_bf16(const float* a, const bf16_t* b, bf16_t* out, int64_t n,
                            hipStream_t st) {
   if (n % 8 != 0) return hipErrorInvalidValue;
   const int64_t n8 = n / 8;

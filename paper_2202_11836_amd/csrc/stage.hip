@@ -84,12 +84,12 @@ __global__ void fill_kernel(float* out, int64_t n, float v) {
   if (i < n) out[i] = v;
 }
 
-// out = bf (bf16) or a + b (fp32), as fp32.
-__global__ void grad_record_kernel(const bf16_t* bf, const float* a, const float* b, float* out,
+// out = bf (bf16), or a (fp32) + b (bf16, may be null), as fp32.
+__global__ void grad_record_kernel(const bf16_t* bf, const float* a, const bf16_t* b, float* out,
                                    int64_t n) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
-  out[i] = bf ? bf2f(bf[i]) : a[i] + (b ? b[i] : 0.0f);
+  out[i] = bf ? bf2f(bf[i]) : a[i] + (b ? bf2f(b[i]) : 0.0f);
 }
 
 __global__ void ones_u8_kernel(uint8_t* out, int64_t n) {
@@ -172,6 +172,7 @@ struct stage {
   void* dY = nullptr;       // [T, h] gradient flowing between layers (fp32 stages)
   float* dz1f = nullptr;    // [T, h] fp32 dZ1, residual branch of dX (bf16 stages)
   float* dz2f = nullptr;    // [T, h] fp32 dZ2, residual branch of dH1 (bf16 stages)
+  void* prod = nullptr;     // [T, h] bf16 data-gradient GEMM product joining them (bf16 stages)
   float* part = nullptr;    // column-sum partials
   float* part2 = nullptr;   // second LayerNorm's partials (bf16: reduced at the layer's end)
   float* colpart_ffn = nullptr;  // [ceil(T/128), f] column sums of dU (bf16 stages)
@@ -452,11 +453,12 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
       (st = A(&s->dU, T * f * e)) || (st = A(&s->dZ1, T * h * e)) || (st = A(&s->dC, T * h * e)))
     return st;
   // The gradient between layers and at H1: in the stage dtype on fp32
-  // stages; on bf16 stages the fp32 residual branches dZ1 and dZ2 (the GEMM
-  // products go through tmp).
+  // stages; on bf16 stages the fp32 residual branches dZ1 and dZ2 and the
+  // bf16 GEMM product added to them.
   if (s->dtype == STAGE_F32 ? ((st = A(&s->dH1, T * h * e)) || (st = A(&s->dY, T * h * e)))
                             : ((st = A((void**)&s->dz1f, T * h * 4)) ||
-                               (st = A((void**)&s->dz2f, T * h * 4))))
+                               (st = A((void**)&s->dz2f, T * h * 4)) ||
+                               (st = A(&s->prod, T * h * e))))
     return st;
   const int64_t nqb = ((int64_t)S + 31) / 32;
   if ((st = A((void**)&s->colpart_ffn, ((T + 127) / 128) * f * 4)) ||
@@ -711,7 +713,7 @@ stage_status col_sum(stage_t* s, int site, int site_red, const T* x, int n, floa
 }
 
 // Records the gradient reaching layer l's output when recording is on.
-stage_status record_grad(stage_t* s, int l, const bf16_t* bf, const float* a, const float* b) {
+stage_status record_grad(stage_t* s, int l, const bf16_t* bf, const float* a, const bf16_t* b) {
   if (!s->record_grads || (int)s->rec.size() != s->L) return STAGE_OK;
   const int64_t n = (int64_t)s->B * s->S * s->h;
   hipLaunchKernelGGL(grad_record_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
@@ -865,14 +867,15 @@ stage_status backward_f32(stage_t* s, const float* dy, float* dx) {
 
 // Gradient reaching a LayerNorm of a bf16 stage: the caller's bf16 tensor
 // (at the stage's top, or below a stage boundary), or the fp32 sum of the
-// residual branch and the data-gradient GEMM's product.  The backward
-// residual stream stays in fp32 inside a stage: rounding it to bf16 at each
-// of a layer's two residual additions is what the gradient error of a deep
-// stage grows from.
+// residual branch (fp32) and the data-gradient GEMM's product (bf16).  The
+// backward residual stream stays in fp32 inside a stage: rounding it to
+// bf16 at each of a layer's two residual additions is what the gradient
+// error of a deep stage grows from (the product's own rounding is not: it
+// enters the stream once).
 struct GradIn {
   const bf16_t* bf;
   const float* a;
-  const float* b;
+  const bf16_t* b;
 };
 
 // Backward of a bf16 stage.  Per layer: the LayerNorm backward kernels take
@@ -942,17 +945,17 @@ stage_status backward_bf16(stage_t* s, const bf16_t* dy, bf16_t* dx) {
                            {gr[STAGE_B_1], nullptr, nullptr, nullptr}};
       // dW_1 = dU^T H1
       wjobs[nw++] = {dU, f, v.H1, h, f, h, gr[STAGE_W_1]};
-      // dH1 = dZ2 + dU W_1: the product in fp32, the sum in the first
+      // dH1 = dZ2 + dU W_1: the product in bf16, the sum in the first
       // LayerNorm's backward (or here, rounded, when this half is the
       // stage's first unit and dH1 is its dx)
       {
-        GemmArgs g = gemm_args(dU, f, s->wt_1, f, s->tmp, h, Tn, h, f);
-        SITE(FFN1_DGRAD, gemm_bf16(g, true, true, EPI_STORE, true, 1, st));
+        GemmArgs g = gemm_args(dU, f, s->wt_1, f, s->prod, h, Tn, h, f);
+        SITE(FFN1_DGRAD, gemm_bf16(g, true, true, EPI_STORE, false, 1, st));
       }
       if (attn) {
-        gh1 = GradIn{nullptr, s->dz2f, s->tmp};
+        gh1 = GradIn{nullptr, s->dz2f, (const T*)s->prod};
       } else {
-        HIPCK(add_f32_to_bf16(s->dz2f, s->tmp, dx, (int64_t)Tn * h, st));
+        HIPCK(add_f32_to_bf16(s->dz2f, (const T*)s->prod, dx, (int64_t)Tn * h, st));
       }
     }  // feed-forward half
     if (attn) {
@@ -981,16 +984,16 @@ stage_status backward_bf16(stage_t* s, const bf16_t* dy, bf16_t* dx) {
                            {gr[STAGE_B_QKV], nullptr, nullptr, nullptr}};
       // dW_qkv = dQKV^T X
       wjobs[nw++] = {dQKV, 3 * h, v.X, h, 3 * h, h, gr[STAGE_W_QKV]};
-      // dX = dZ1 + dQKV W_qkv: the product in fp32; the sum in the previous
+      // dX = dZ1 + dQKV W_qkv: the product in bf16; the sum in the previous
       // layer's second LayerNorm backward, or here, rounded, for the stage's dx
       {
-        GemmArgs g = gemm_args(dQKV, 3 * h, s->wt_qkv, 3 * h, s->tmp, h, Tn, h, 3 * h);
-        SITE(QKV_DGRAD, gemm_bf16(g, true, true, EPI_STORE, true, 1, st));
+        GemmArgs g = gemm_args(dQKV, 3 * h, s->wt_qkv, 3 * h, s->prod, h, Tn, h, 3 * h);
+        SITE(QKV_DGRAD, gemm_bf16(g, true, true, EPI_STORE, false, 1, st));
       }
       if (l > 0) {
-        gin = GradIn{nullptr, s->dz1f, s->tmp};
+        gin = GradIn{nullptr, s->dz1f, (const T*)s->prod};
       } else {
-        HIPCK(add_f32_to_bf16(s->dz1f, s->tmp, dx, (int64_t)Tn * h, st));
+        HIPCK(add_f32_to_bf16(s->dz1f, (const T*)s->prod, dx, (int64_t)Tn * h, st));
       }
     }
     if ((r = wgrad_group(s, wjobs, nw, cjobs, nc))) return r;
