@@ -124,7 +124,8 @@ stage_status stage_init(int L_stage, int hidden, int heads, int ffn, uint64_t se
  * of L layers, except that on bf16 stages the tensors that cross a stage
  * boundary are rounded to bf16 there (they are the stage's input and output
  * in its dtype): an H1 that crosses a boundary reaches the second LayerNorm
- * rounded (inside a stage it is added in fp32), and in the backward pass the
+ * rounded (inside a stage it is added with its rounding residual, to about
+ * 16 significant bits), and in the backward pass the
  * gradient that crosses a boundary is rounded (inside a stage the residual
  * stream of the backward pass stays in fp32).  Weights are drawn as in stage_init with the global
  * layer index, so a layer has the same weights in every stage that holds

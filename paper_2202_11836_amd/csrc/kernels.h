@@ -108,13 +108,14 @@ hipError_t wgrad_group_reduce(const GemmArgs* p, float* const* out, int n, const
 // ---------------------------------------------------------------------------
 // Row kernels (one wavefront per row), T = float or bf16_t.
 // ---------------------------------------------------------------------------
-// z = a + bias + resid;  y = gamma * xhat + beta with xhat = (z - mean) * rstd.
-// a is the fp32 output of the preceding GEMM; y32 (optional, may be null)
-// receives y in fp32 as well.
-template <typename T, typename TA, typename TR>
-hipError_t add_ln_fwd(const TA* a, const float* bias, const TR* resid, const float* gamma,
-                      const float* beta, T* y, float* y32, T* xhat, float* rstd, int rows, int h,
-                      hipStream_t st);
+// z = a + bias + resid (+ resid_lo);  y = gamma * xhat + beta with
+// xhat = (z - mean) * rstd.  a is the fp32 output of the preceding GEMM;
+// resid_lo (optional, may be null) is the rounding residual of resid; ylo
+// (optional, may be null) receives y - y as stored, in T.
+template <typename T, typename TA>
+hipError_t add_ln_fwd(const TA* a, const float* bias, const T* resid, const T* resid_lo,
+                      const float* gamma, const float* beta, T* y, T* ylo, T* xhat, float* rstd,
+                      int rows, int h, hipStream_t st);
 
 // dz = rstd * (g - mean(g) - xhat * mean(g * xhat)), g = dy * gamma.
 // Column partial sums per block of LN_BWD_RPB rows (ln_bwd_blocks(rows)
@@ -126,16 +127,17 @@ template <typename T>
 hipError_t ln_bwd(const T* dy, const T* xhat, const float* rstd, const float* gamma, T* dz,
                   float* part, int rows, int h, hipStream_t st);
 
-// bf16 stages: the same with dy either one bf16 tensor (dya = dyb = null)
-// or the sum dya + dyb of an fp32 and a bf16 tensor, in fp32 (dy = null);
-// dz in bf16 and, when dz32 is not null, in fp32 as well.  Partials as
-// ln_bwd.
-hipError_t ln_bwd_bf16(const bf16_t* dy, const float* dya, const bf16_t* dyb, const bf16_t* xhat,
-                       const float* rstd, const float* gamma, bf16_t* dz, float* dz32,
-                       float* part, int rows, int h, hipStream_t st);
-// out = bf16(a + b), a fp32, b bf16, n elements (a multiple of 8).
-hipError_t add_f32_to_bf16(const float* a, const bf16_t* b, bf16_t* out, int64_t n,
-                           hipStream_t st);
+// bf16 stages: the same with dy either one bf16 tensor (ahi = alo = b =
+// null) or the fp32 sum (ahi + alo) + b of three bf16 tensors (dy = null):
+// a residual branch carried as its bf16 rounding and rounding residual,
+// plus a bf16 GEMM product.  dz in bf16 and, when dzlo is not null, dz's
+// bf16 rounding residual.  Partials as ln_bwd.
+hipError_t ln_bwd_bf16(const bf16_t* dy, const bf16_t* ahi, const bf16_t* alo, const bf16_t* b,
+                       const bf16_t* xhat, const float* rstd, const float* gamma, bf16_t* dz,
+                       bf16_t* dzlo, float* part, int rows, int h, hipStream_t st);
+// out = bf16((ahi + alo) + b), all bf16, n elements (a multiple of 8).
+hipError_t add3_bf16(const bf16_t* ahi, const bf16_t* alo, const bf16_t* b, bf16_t* out,
+                     int64_t n, hipStream_t st);
 
 // dst[c][r] = src[r][c] for a bf16 [R][C] matrix.
 // dst[c][r] = src[r][c] for up to TRANSPOSE_MAX_JOBS row-major R x C bf16

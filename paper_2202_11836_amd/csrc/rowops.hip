@@ -49,14 +49,19 @@ __device__ __forceinline__ float as_stored(float v, const bf16_t*) { return bf2f
 __device__ __forceinline__ float as_stored(float v, const float*) { return v; }
 
 // One wavefront per row.  Lane `lane` owns the 8-column chunks
-// c = lane + 64 i (i < NC, c < h / 8).
-template <typename T, typename TA, typename TR, int NC>
+// c = lane + 64 i (i < NC, c < h / 8).  The residual is resid, plus
+// resid_lo when not null (a value carried as its bf16 rounding and the
+// rounding residual); ylo, when not null, receives y's rounding residual
+// y - bf16(y) in bf16, so that y + ylo carries y to about 16 significant
+// bits.
+template <typename T, typename TA, int NC>
 __global__ __launch_bounds__(256) void add_ln_fwd_kernel(const TA* __restrict__ a,
                                                          const float* __restrict__ bias,
-                                                         const TR* __restrict__ resid,
+                                                         const T* __restrict__ resid,
+                                                         const T* __restrict__ resid_lo,
                                                          const float* __restrict__ gamma,
                                                          const float* __restrict__ beta,
-                                                         T* __restrict__ y, float* __restrict__ y32,
+                                                         T* __restrict__ y, T* __restrict__ ylo,
                                                          T* __restrict__ xhat,
                                                          float* __restrict__ rstd, int rows, int h) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -70,10 +75,15 @@ __global__ __launch_bounds__(256) void add_ln_fwd_kernel(const TA* __restrict__ 
   for (int i = 0; i < NC; ++i) {
     const int c = lane + 64 * i;
     if (c < nchunk) {
-      float av[8], rv[8], bv[8];
+      float av[8], rv[8], bv[8], lv[8];
       load8(a + base + 8 * c, av);
       load8(resid + base + 8 * c, rv);
       load8(bias + 8 * c, bv);
+      if (resid_lo) {
+        load8(resid_lo + base + 8 * c, lv);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) rv[k] += lv[k];
+      }
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         z[i][k] = av[k] + bv[k] + rv[k];
@@ -109,7 +119,11 @@ __global__ __launch_bounds__(256) void add_ln_fwd_kernel(const TA* __restrict__ 
       }
       store8(xhat + base + 8 * c, xh);
       store8(y + base + 8 * c, yv);
-      if (y32) store8(y32 + base + 8 * c, yv);
+      if (ylo) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) yv[k] -= as_stored(yv[k], y);
+        store8(ylo + base + 8 * c, yv);
+      }
     }
   }
   if (lane == 0) rstd[row] = r;
@@ -236,19 +250,21 @@ __device__ __forceinline__ float bf_at(const u32x4_t& r, int k) {
   return (k & 1) ? bf_hi(r[k >> 1]) : bf_lo(r[k >> 1]);
 }
 
-// The incoming gradient dy is either one bf16 tensor or, when SUM32, the
-// sum dya + dyb of an fp32 and a bf16 tensor (the backward residual stream
-// of a bf16 stage: the fp32 gradient of the residual branch plus the bf16
-// product of the data-gradient GEMM, so that the stream itself is never
-// rounded to bf16).
-// dz goes out in bf16 (the operand of the following GEMMs) and, when dz32
-// is not null, in fp32 as well (the residual branch of the next addition).
-template <int NC, bool SUM32>
+// The incoming gradient dy is either one bf16 tensor or, when SUM3, the
+// fp32 sum (ahi + alo) + b of three bf16 tensors: the backward residual
+// stream of a bf16 stage, i.e. the residual branch carried as its bf16
+// rounding ahi plus the rounding residual alo (about 16 significant bits),
+// plus the bf16 product b of the data-gradient GEMM, so that the stream
+// itself is never rounded to bf16.
+// dz goes out in bf16 (the operand of the following GEMMs) and, when dzlo
+// is not null, its rounding residual dz - bf16(dz) in bf16 as well (the
+// residual branch of the next addition).
+template <int NC, bool SUM3>
 __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(
-    const bf16_t* __restrict__ dy, const float* __restrict__ dya, const bf16_t* __restrict__ dyb,
-    const bf16_t* __restrict__ xhat, const float* __restrict__ rstd,
-    const float* __restrict__ gamma, bf16_t* __restrict__ dz, float* __restrict__ dz32,
-    float* __restrict__ part, int rows, int h, int rpb) {
+    const bf16_t* __restrict__ dy, const bf16_t* __restrict__ ahi, const bf16_t* __restrict__ alo,
+    const bf16_t* __restrict__ dyb, const bf16_t* __restrict__ xhat,
+    const float* __restrict__ rstd, const float* __restrict__ gamma, bf16_t* __restrict__ dz,
+    bf16_t* __restrict__ dzlo, float* __restrict__ part, int rows, int h, int rpb) {
   extern __shared__ float red[];  // [4 wavefronts][3][h]
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
@@ -266,10 +282,8 @@ __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(
   const int r1 = min(rows, r0 + rpb);
   const float inv_h = 1.0f / (float)h;
   for (int row0 = r0 + wave; row0 < r1; row0 += 8) {
-    // SUM32: the fp32 addend as two 16-byte halves and the bf16 addend
-    // packed; else dy packed bf16
-    u32x4_t dr[2][NC], xr[2][NC];
-    f32x4_t fa[2][NC][2];
+    // dy packed bf16 (SUM3: the product b, with ahi and alo beside it)
+    u32x4_t dr[2][NC], xr[2][NC], hr[2][NC], lr[2][NC];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int row = row0 + 4 * u;
@@ -278,25 +292,24 @@ __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(
       for (int i = 0; i < NC; ++i) {
         const int c = lane + 64 * i;
         if (c < nchunk && row < r1) {
-          if constexpr (SUM32) {
-            fa[u][i][0] = *(const f32x4_t*)(dya + base + 8 * c);
-            fa[u][i][1] = *(const f32x4_t*)(dya + base + 8 * c + 4);
+          if constexpr (SUM3) {
+            hr[u][i] = *(const u32x4_t*)(ahi + base + 8 * c);
+            lr[u][i] = *(const u32x4_t*)(alo + base + 8 * c);
             dr[u][i] = *(const u32x4_t*)(dyb + base + 8 * c);
           } else {
             dr[u][i] = *(const u32x4_t*)(dy + base + 8 * c);
           }
           xr[u][i] = *(const u32x4_t*)(xhat + base + 8 * c);
         } else {
-          if constexpr (SUM32) fa[u][i][0] = fa[u][i][1] = f32x4_t{0, 0, 0, 0};
-          dr[u][i] = u32x4_t{0, 0, 0, 0};
+          hr[u][i] = lr[u][i] = dr[u][i] = u32x4_t{0, 0, 0, 0};
           xr[u][i] = u32x4_t{0, 0, 0, 0};
         }
       }
     }
     // the incoming gradient at (u, i, k)
     auto dyv = [&](int u, int i, int k) -> float {
-      if constexpr (SUM32)
-        return fa[u][i][k >> 2][k & 3] + bf_at(dr[u][i], k);
+      if constexpr (SUM3)
+        return (bf_at(hr[u][i], k) + bf_at(lr[u][i], k)) + bf_at(dr[u][i], k);
       else
         return bf_at(dr[u][i], k);
     };
@@ -345,9 +358,12 @@ __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(
             pz[i][2 * k2 + 1] += bf_hi(o[k2]);
           }
           *(u32x4_t*)(dz + base + 8 * c) = o;
-          if (dz32) {
-            *(f32x4_t*)(dz32 + base + 8 * c) = f32x4_t{dd[0], dd[1], dd[2], dd[3]};
-            *(f32x4_t*)(dz32 + base + 8 * c + 4) = f32x4_t{dd[4], dd[5], dd[6], dd[7]};
+          if (dzlo) {
+            u32x4_t lo;
+#pragma unroll
+            for (int k2 = 0; k2 < 4; ++k2)
+              lo[k2] = pack_bf16x2(dd[2 * k2] - bf_lo(o[k2]), dd[2 * k2 + 1] - bf_hi(o[k2]));
+            *(u32x4_t*)(dzlo + base + 8 * c) = lo;
           }
         }
       }
@@ -373,19 +389,21 @@ __global__ __launch_bounds__(256, (NC <= 2 ? 2 : 1)) void ln_bwd_bf16_kernel(
     P[e] = ((red[e] + red[3 * h + e]) + red[6 * h + e]) + red[9 * h + e];
 }
 
-// out = a + b rounded to bf16 (a fp32, b bf16), 8 elements per thread
+// out = (ahi + alo) + b rounded to bf16 (all bf16), 8 elements per thread
 // (n % 8 == 0).
-__global__ __launch_bounds__(256) void add_f32_to_bf16_kernel(const float* __restrict__ a,
-                                                              const bf16_t* __restrict__ b,
-                                                              bf16_t* __restrict__ out, int64_t n8) {
+__global__ __launch_bounds__(256) void add3_bf16_kernel(const bf16_t* __restrict__ ahi,
+                                                        const bf16_t* __restrict__ alo,
+                                                        const bf16_t* __restrict__ b,
+                                                        bf16_t* __restrict__ out, int64_t n8) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= n8) return;
-  float va[8], vb[8];
-  load8(a + 8 * i, va);
+  float vh[8], vl[8], vb[8];
+  load8(ahi + 8 * i, vh);
+  load8(alo + 8 * i, vl);
   load8(b + 8 * i, vb);
 #pragma unroll
-  for (int k = 0; k < 8; ++k) va[k] += vb[k];
-  store8(out + 8 * i, va);
+  for (int k = 0; k < 8; ++k) vh[k] = (vh[k] + vl[k]) + vb[k];
+  store8(out + 8 * i, vh);
 }
 
 template <typename T>
@@ -524,17 +542,17 @@ hipError_t transpose_bf16(const TransposeJob* jobs, int n, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <typename T, typename TA, typename TR>
-hipError_t add_ln_fwd(const TA* a, const float* bias, const TR* resid, const float* gamma,
-                      const float* beta, T* y, float* y32, T* xhat, float* rstd, int rows, int h,
-                      hipStream_t st) {
+template <typename T, typename TA>
+hipError_t add_ln_fwd(const TA* a, const float* bias, const T* resid, const T* resid_lo,
+                      const float* gamma, const float* beta, T* y, T* ylo, T* xhat, float* rstd,
+                      int rows, int h, hipStream_t st) {
   if (h % 64 != 0 || h > 2048) return hipErrorInvalidValue;
   if (rows <= 0) return hipSuccess;
   const int nc = (h / 8 + 63) / 64;
   dim3 grid((rows + 3) / 4), blk(256);
 #define LAUNCH_LN(NCV)                                                                        \
-  hipLaunchKernelGGL((add_ln_fwd_kernel<T, TA, TR, NCV>), grid, blk, 0, st, a, bias, resid, gamma, \
-                     beta, y, y32, xhat, rstd, rows, h)
+  hipLaunchKernelGGL((add_ln_fwd_kernel<T, TA, NCV>), grid, blk, 0, st, a, bias, resid, resid_lo, \
+                     gamma, beta, y, ylo, xhat, rstd, rows, h)
   switch (nc) {
     case 1: LAUNCH_LN(1); break;
     case 2: LAUNCH_LN(2); break;
@@ -547,20 +565,21 @@ hipError_t add_ln_fwd(const TA* a, const float* bias, const TR* resid, const flo
 
 int ln_bwd_blocks(int rows) { return (rows + LN_BWD_RPB - 1) / LN_BWD_RPB; }
 
-hipError_t ln_bwd_bf16(const bf16_t* dy, const float* dya, const bf16_t* dyb, const bf16_t* xhat,
-                       const float* rstd, const float* gamma, bf16_t* dz, float* dz32,
-                       float* part, int rows, int h, hipStream_t st) {
+hipError_t ln_bwd_bf16(const bf16_t* dy, const bf16_t* ahi, const bf16_t* alo, const bf16_t* b,
+                       const bf16_t* xhat, const float* rstd, const float* gamma, bf16_t* dz,
+                       bf16_t* dzlo, float* part, int rows, int h, hipStream_t st) {
   if (h % 64 != 0 || h > 2048) return hipErrorInvalidValue;
-  if ((dy == nullptr) == (dya == nullptr || dyb == nullptr)) return hipErrorInvalidValue;
+  const bool sum3 = ahi && alo && b;
+  if ((dy == nullptr) == !sum3) return hipErrorInvalidValue;
   if (rows <= 0) return hipSuccess;
   const int nc = (h / 8 + 63) / 64;
   dim3 grid(ln_bwd_blocks(rows)), blk(256);
   size_t sh = (size_t)4 * 3 * h * sizeof(float);
   const int rpb = LN_BWD_RPB;
-#define LAUNCH_LNB(NCV, S32)                                                                  \
-  hipLaunchKernelGGL((ln_bwd_bf16_kernel<NCV, S32>), grid, blk, sh, st, dy, dya, dyb, xhat, rstd, \
-                     gamma, dz, dz32, part, rows, h, rpb)
-  if (dy) {
+#define LAUNCH_LNB(NCV, S3)                                                                   \
+  hipLaunchKernelGGL((ln_bwd_bf16_kernel<NCV, S3>), grid, blk, sh, st, dy, ahi, alo, b, xhat,  \
+                     rstd, gamma, dz, dzlo, part, rows, h, rpb)
+  if (!sum3) {
     switch (nc) {
       case 1: LAUNCH_LNB(1, false); break;
       case 2: LAUNCH_LNB(2, false); break;
@@ -579,13 +598,13 @@ hipError_t ln_bwd_bf16(const bf16_t* dy, const float* dya, const bf16_t* dyb, co
   return hipGetLastError();
 }
 
-hipError_t add_f32_to_bf16(const float* a, const bf16_t* b, bf16_t* out, int64_t n,
-                           hipStream_t st) {
+hipError_t add3_bf16(const bf16_t* ahi, const bf16_t* alo, const bf16_t* b, bf16_t* out,
+                     int64_t n, hipStream_t st) {
   if (n % 8 != 0) return hipErrorInvalidValue;
   const int64_t n8 = n / 8;
   if (n8 == 0) return hipSuccess;
-  hipLaunchKernelGGL(add_f32_to_bf16_kernel, dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0, st,
-                     a, b, out, n8);
+  hipLaunchKernelGGL(add3_bf16_kernel, dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0, st, ahi,
+                     alo, b, out, n8);
   return hipGetLastError();
 }
 
@@ -599,7 +618,8 @@ hipError_t ln_bwd(const T* dy, const T* xhat, const float* rstd, const float* ga
   size_t sh = (size_t)4 * 3 * h * sizeof(float);
   const int rpb = LN_BWD_RPB;
   if constexpr (std::is_same<T, bf16_t>::value) {
-    return ln_bwd_bf16(dy, nullptr, nullptr, xhat, rstd, gamma, dz, nullptr, part, rows, h, st);
+    return ln_bwd_bf16(dy, nullptr, nullptr, nullptr, xhat, rstd, gamma, dz, nullptr, part, rows,
+                       h, st);
   }
   switch (nc) {
     case 1: hipLaunchKernelGGL((ln_bwd_kernel<T, 1>), grid, blk, sh, st, dy, xhat, rstd, gamma, dz, part, rows, h, rpb); break;
@@ -651,9 +671,9 @@ hipError_t softmax_bwd(const float* dP, const T* P, T* dS, int BH, int S, int ld
 }
 
 #define INST(T)                                                                                 \
-  template hipError_t add_ln_fwd<T, float, T>(const float*, const float*, const T*,            \
-                                              const float*, const float*, T*, float*, T*,     \
-                                              float*, int, int, hipStream_t);                 \
+  template hipError_t add_ln_fwd<T, float>(const float*, const float*, const T*, const T*,     \
+                                           const float*, const float*, T*, T*, T*, float*,    \
+                                           int, int, hipStream_t);                            \
   template hipError_t ln_bwd<T>(const T*, const T*, const float*, const float*, T*, float*,    \
                                 int, int, hipStream_t);                                        \
   template hipError_t col_partial<T>(const T*, int, int, float*, int, hipStream_t);            \
@@ -663,7 +683,3 @@ hipError_t softmax_bwd(const float* dP, const T* P, T* dS, int BH, int S, int ld
                                      hipStream_t);
 INST(float)
 INST(bf16_t)
-template hipError_t add_ln_fwd<bf16_t, float, float>(const float*, const float*, const float*,
-                                                       const float*, const float*, bf16_t*,
-                                                       float*, bf16_t*, float*, int, int,
-                                                       hipStream_t);

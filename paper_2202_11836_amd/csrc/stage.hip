@@ -84,12 +84,12 @@ __global__ void fill_kernel(float* out, int64_t n, float v) {
   if (i < n) out[i] = v;
 }
 
-// out = bf (bf16), or a (fp32) + b (bf16, may be null), as fp32.
-__global__ void grad_record_kernel(const bf16_t* bf, const float* a, const bf16_t* b, float* out,
-                                   int64_t n) {
+// out = x (fp32; fp32 stages), or bf (bf16), or (hi + lo) + b (bf16), as fp32.
+__global__ void grad_record_kernel(const float* x, const bf16_t* bf, const bf16_t* hi,
+                                   const bf16_t* lo, const bf16_t* b, float* out, int64_t n) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
-  out[i] = bf ? bf2f(bf[i]) : a[i] + (b ? bf2f(b[i]) : 0.0f);
+  out[i] = x ? x[i] : bf ? bf2f(bf[i]) : (bf2f(hi[i]) + bf2f(lo[i])) + bf2f(b[i]);
 }
 
 __global__ void ones_u8_kernel(uint8_t* out, int64_t n) {
@@ -158,7 +158,7 @@ struct stage {
   std::vector<Saved> saved;
   uint8_t* mask = nullptr;
   float* tmp = nullptr;     // [T, h] fp32 GEMM output before LayerNorm
-  float* h1f = nullptr;     // [T, h] fp32 copy of H1 (bf16 stages)
+  void* h1lo = nullptr;     // [T, h] H1's bf16 rounding residual (bf16 stages)
   float* scores = nullptr;  // [B*H, S, S] fp32 (scores, then dP; fp32 stages)
   int* kext = nullptr;      // [B] key extent of each sequence
   float* dsum = nullptr;    // [B*H, S] rowsum(dO * O) (bf16 stages)
@@ -170,8 +170,10 @@ struct stage {
   void* dZ1 = nullptr;      // [T, h]
   void* dC = nullptr;       // [T, h]
   void* dY = nullptr;       // [T, h] gradient flowing between layers (fp32 stages)
-  float* dz1f = nullptr;    // [T, h] fp32 dZ1, residual branch of dX (bf16 stages)
-  float* dz2f = nullptr;    // [T, h] fp32 dZ2, residual branch of dH1 (bf16 stages)
+  // bf16 stages: the rounding residuals of dZ1 and dZ2 (with the bf16 dZ1,
+  // dZ2 they carry the residual branches of dX and dH1 to ~16 bits)
+  void* dz1lo = nullptr;    // [T, h]
+  void* dz2lo = nullptr;    // [T, h]
   void* prod = nullptr;     // [T, h] bf16 data-gradient GEMM product joining them (bf16 stages)
   float* part = nullptr;    // column-sum partials
   float* part2 = nullptr;   // second LayerNorm's partials (bf16: reduced at the layer's end)
@@ -446,18 +448,17 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
       return st;
   }
   if ((st = A((void**)&s->mask, T)) || (st = A((void**)&s->tmp, T * h * 4)) ||
-      (st = A((void**)&s->h1f, T * h * 4)) ||
+      (st = A(&s->h1lo, T * h * e)) ||
       (st = A((void**)&s->scores, BSS * 4)) || (st = A(&s->dS, BSS * e)) ||
       (st = A((void**)&s->kext, (size_t)B * 4)) || (st = A((void**)&s->dsum, BHS * 4)) ||
       (st = A(&s->dQKV, T * 3 * h * e)) || (st = A(&s->dZ2, T * h * e)) ||
       (st = A(&s->dU, T * f * e)) || (st = A(&s->dZ1, T * h * e)) || (st = A(&s->dC, T * h * e)))
     return st;
   // The gradient between layers and at H1: in the stage dtype on fp32
-  // stages; on bf16 stages the fp32 residual branches dZ1 and dZ2 and the
-  // bf16 GEMM product added to them.
+  // stages; on bf16 stages the rounding residuals of the residual branches
+  // dZ1 and dZ2 and the bf16 GEMM product added to them.
   if (s->dtype == STAGE_F32 ? ((st = A(&s->dH1, T * h * e)) || (st = A(&s->dY, T * h * e)))
-                            : ((st = A((void**)&s->dz1f, T * h * 4)) ||
-                               (st = A((void**)&s->dz2f, T * h * 4)) ||
+                            : ((st = A(&s->dz1lo, T * h * e)) || (st = A(&s->dz2lo, T * h * e)) ||
                                (st = A(&s->prod, T * h * e))))
     return st;
   const int64_t nqb = ((int64_t)S + 31) / 32;
@@ -600,11 +601,12 @@ stage_status forward_impl(stage_t* s, const T* x, T* y) {
   for (int l = 0; l < s->L; ++l) {
     Saved& v = s->saved[l];
     auto& p = s->param[l];
-    // For bf16 stages H1 is also written in fp32 when this stage computes
-    // it: it is the residual of the second LayerNorm, so its rounding to
-    // bf16 stays out of Y.  (A stage that starts at a feed-forward half
-    // receives H1 in bf16, as the previous stage's output.)
-    float* h1_32 = (std::is_same<T, float>::value || !has_attn(s, l)) ? nullptr : s->h1f;
+    // For bf16 stages the first LayerNorm also writes H1's bf16 rounding
+    // residual when this stage computes H1: H1 is the residual of the
+    // second LayerNorm, which adds it back, so H1's rounding to bf16 stays
+    // out of Y.  (A stage that starts at a feed-forward half receives H1 in
+    // bf16, as the previous stage's output.)
+    T* h1_lo = (std::is_same<T, float>::value || !has_attn(s, l)) ? nullptr : (T*)s->h1lo;
     if (has_attn(s, l)) {
       const T* X = (const T*)v.X;
       T* QKV = (T*)v.QKV;
@@ -652,11 +654,11 @@ stage_status forward_impl(stage_t* s, const T* x, T* y) {
       // The last layer of a stage that ends at an attention half writes H1
       // straight to the stage output.
       const bool to_out = !has_ffn(s, l);
-      if (to_out) h1_32 = nullptr;
-      SITE(LN1_FWD, add_ln_fwd<T, float, T>(s->tmp, (const float*)p[STAGE_B_O], X,
-                                     (const float*)p[STAGE_G1], (const float*)p[STAGE_BE1],
-                                     to_out ? y : (T*)v.H1, h1_32, (T*)v.xhat1, v.rstd1, Tn, h,
-                                     st));
+      if (to_out) h1_lo = nullptr;
+      SITE(LN1_FWD, add_ln_fwd<T, float>(s->tmp, (const float*)p[STAGE_B_O], X, nullptr,
+                                         (const float*)p[STAGE_G1], (const float*)p[STAGE_BE1],
+                                         to_out ? y : (T*)v.H1, h1_lo, (T*)v.xhat1, v.rstd1, Tn,
+                                         h, st));
       if (to_out) break;
     }  // attention half
     // U = H1 W_1^T + b_1;  G = GELU(U) and GELU'(U) (kept for the backward)
@@ -672,15 +674,10 @@ stage_status forward_impl(stage_t* s, const T* x, T* y) {
       SITE(FFN2_FWD, Gemm<T>::run(g, true, true, EPI_STORE, true, 1, st));
     }
     T* Y = (l + 1 < s->L) ? (T*)s->saved[l + 1].X : y;
-    if (h1_32)
-      SITE(LN2_FWD, add_ln_fwd<T, float, float>(s->tmp, (const float*)p[STAGE_B_2], h1_32,
-                                         (const float*)p[STAGE_G2], (const float*)p[STAGE_BE2],
-                                         Y, nullptr, (T*)v.xhat2, v.rstd2, Tn, h, st));
-    else
-      SITE(LN2_FWD, add_ln_fwd<T, float, T>(s->tmp, (const float*)p[STAGE_B_2],
-                                     (const T*)v.H1, (const float*)p[STAGE_G2],
-                                     (const float*)p[STAGE_BE2], Y, nullptr, (T*)v.xhat2,
-                                     v.rstd2, Tn, h, st));
+    SITE(LN2_FWD, add_ln_fwd<T, float>(s->tmp, (const float*)p[STAGE_B_2], (const T*)v.H1,
+                                       h1_lo, (const float*)p[STAGE_G2],
+                                       (const float*)p[STAGE_BE2], Y, nullptr, (T*)v.xhat2,
+                                       v.rstd2, Tn, h, st));
   }
   return STAGE_OK;
 }
@@ -713,11 +710,12 @@ stage_status col_sum(stage_t* s, int site, int site_red, const T* x, int n, floa
 }
 
 // Records the gradient reaching layer l's output when recording is on.
-stage_status record_grad(stage_t* s, int l, const bf16_t* bf, const float* a, const bf16_t* b) {
+stage_status record_grad(stage_t* s, int l, const float* x, const bf16_t* bf, const bf16_t* hi,
+                         const bf16_t* lo, const bf16_t* b) {
   if (!s->record_grads || (int)s->rec.size() != s->L) return STAGE_OK;
   const int64_t n = (int64_t)s->B * s->S * s->h;
   hipLaunchKernelGGL(grad_record_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
-                     s->stream, bf, a, b, s->rec[l], n);
+                     s->stream, x, bf, hi, lo, b, s->rec[l], n);
   HIPCK(hipGetLastError());
   return STAGE_OK;
 }
@@ -749,7 +747,7 @@ stage_status backward_f32(stage_t* s, const float* dy, float* dx) {
     const void* W1 = p[STAGE_W_1];
     const void* W2 = p[STAGE_W_2];
     const bool attn = has_attn(s, l), ffn = has_ffn(s, l);
-    if ((r = record_grad(s, l, nullptr, dYcur, nullptr))) return r;
+    if ((r = record_grad(s, l, dYcur, nullptr, nullptr, nullptr, nullptr))) return r;
     auto dW = [&](int site, int site_red, const T* dYm, int64_t ld_dy, const T* Xn,
                   int64_t ld_x, int M, int N, float* out) -> stage_status {
       return wgrad<T>(s, site, site_red, dYm, ld_dy, Xn, ld_x, M, N, Tn, out);
@@ -867,14 +865,16 @@ stage_status backward_f32(stage_t* s, const float* dy, float* dx) {
 
 // Gradient reaching a LayerNorm of a bf16 stage: the caller's bf16 tensor
 // (at the stage's top, or below a stage boundary), or the fp32 sum of the
-// residual branch (fp32) and the data-gradient GEMM's product (bf16).  The
-// backward residual stream stays in fp32 inside a stage: rounding it to
-// bf16 at each of a layer's two residual additions is what the gradient
-// error of a deep stage grows from (the product's own rounding is not: it
-// enters the stream once).
+// residual branch, carried as its bf16 rounding hi plus the rounding
+// residual lo (about 16 significant bits), and the data-gradient GEMM's
+// bf16 product b.  The backward residual stream keeps that precision inside
+// a stage: rounding it to bf16 at each of a layer's two residual additions
+// is what the gradient error of a deep stage grows from (the product's own
+// rounding is not: it enters the stream once).
 struct GradIn {
   const bf16_t* bf;
-  const float* a;
+  const bf16_t* hi;
+  const bf16_t* lo;
   const bf16_t* b;
 };
 
@@ -892,7 +892,7 @@ stage_status backward_bf16(stage_t* s, const bf16_t* dy, bf16_t* dx) {
   const int Tn = B * S;
   hipStream_t st = s->stream;
   stage_status r;
-  GradIn gin{dy, nullptr, nullptr};
+  GradIn gin{dy, nullptr, nullptr, nullptr};
   for (int l = s->L - 1; l >= 0; --l) {
     Saved& v = s->saved[l];
     auto& p = s->param[l];
@@ -903,7 +903,7 @@ stage_status backward_bf16(stage_t* s, const bf16_t* dy, bf16_t* dx) {
     T* dC = (T*)s->dC;
     T* dQKV = (T*)s->dQKV;
     const bool attn = has_attn(s, l), ffn = has_ffn(s, l);
-    if ((r = record_grad(s, l, gin.bf, gin.a, gin.b))) return r;
+    if ((r = record_grad(s, l, nullptr, gin.bf, gin.hi, gin.lo, gin.b))) return r;
     WgradJob wjobs[GEMM_GROUP_MAX];
     int nw = 0;
     ColJob cjobs[COLJOB_MAX];
@@ -926,8 +926,9 @@ stage_status backward_bf16(stage_t* s, const bf16_t* dy, bf16_t* dx) {
     GradIn gh1 = gin;
     if (ffn) {
       // Y = LN(Z2): dZ2 (bf16 and fp32), dgamma2, dbeta2, db_2 = sum_t dZ2
-      SITE(LN2_BWD, ln_bwd_bf16(gin.bf, gin.a, gin.b, (const T*)v.xhat2, v.rstd2,
-                                (const float*)p[STAGE_G2], dZ2, s->dz2f, s->part2, Tn, h, st));
+      SITE(LN2_BWD, ln_bwd_bf16(gin.bf, gin.hi, gin.lo, gin.b, (const T*)v.xhat2, v.rstd2,
+                                (const float*)p[STAGE_G2], dZ2, (T*)s->dz2lo, s->part2, Tn, h,
+                                st));
       cjobs[nc++] = ColJob{s->part2, ln_bwd_blocks(Tn), 3, h,
                            {gr[STAGE_G2], gr[STAGE_BE2], gr[STAGE_B_2], nullptr}};
       // dW_2 = dZ2^T G
@@ -953,15 +954,16 @@ stage_status backward_bf16(stage_t* s, const bf16_t* dy, bf16_t* dx) {
         SITE(FFN1_DGRAD, gemm_bf16(g, true, true, EPI_STORE, false, 1, st));
       }
       if (attn) {
-        gh1 = GradIn{nullptr, s->dz2f, (const T*)s->prod};
+        gh1 = GradIn{nullptr, dZ2, (const T*)s->dz2lo, (const T*)s->prod};
       } else {
-        HIPCK(add_f32_to_bf16(s->dz2f, (const T*)s->prod, dx, (int64_t)Tn * h, st));
+        HIPCK(add3_bf16(dZ2, (const T*)s->dz2lo, (const T*)s->prod, dx, (int64_t)Tn * h, st));
       }
     }  // feed-forward half
     if (attn) {
       // H1 = LN(Z1): dZ1 (bf16 and fp32), dgamma1, dbeta1, db_o
-      SITE(LN1_BWD, ln_bwd_bf16(gh1.bf, gh1.a, gh1.b, (const T*)v.xhat1, v.rstd1,
-                                (const float*)p[STAGE_G1], dZ1, s->dz1f, s->part, Tn, h, st));
+      SITE(LN1_BWD, ln_bwd_bf16(gh1.bf, gh1.hi, gh1.lo, gh1.b, (const T*)v.xhat1, v.rstd1,
+                                (const float*)p[STAGE_G1], dZ1, (T*)s->dz1lo, s->part, Tn, h,
+                                st));
       cjobs[nc++] = ColJob{s->part, ln_bwd_blocks(Tn), 3, h,
                            {gr[STAGE_G1], gr[STAGE_BE1], gr[STAGE_B_O], nullptr}};
       // dW_o = dZ1^T C
@@ -991,9 +993,9 @@ stage_status backward_bf16(stage_t* s, const bf16_t* dy, bf16_t* dx) {
         SITE(QKV_DGRAD, gemm_bf16(g, true, true, EPI_STORE, false, 1, st));
       }
       if (l > 0) {
-        gin = GradIn{nullptr, s->dz1f, (const T*)s->prod};
+        gin = GradIn{nullptr, dZ1, (const T*)s->dz1lo, (const T*)s->prod};
       } else {
-        HIPCK(add_f32_to_bf16(s->dz1f, (const T*)s->prod, dx, (int64_t)Tn * h, st));
+        HIPCK(add3_bf16(dZ1, (const T*)s->dz1lo, (const T*)s->prod, dx, (int64_t)Tn * h, st));
       }
     }
     if ((r = wgrad_group(s, wjobs, nw, cjobs, nc))) return r;
