@@ -50,6 +50,25 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Transposing LDS read ds_read_b64_tr_b16 (gfx950) as inline assembly.
+// With the compiler builtin for it, the compiler first waits for every
+// direct-to-LDS load the wavefront has in flight (vmcnt 0: it cannot tell
+// which LDS bytes they write), which drains a prefetch ring whose next
+// loads were issued just before; the kernels wait for those loads
+// explicitly instead.  The compiler does not track this read either: every
+// result must pass lds_wait() and then lds_hold() before any use, and must
+// stay live until then (its register could otherwise be reused while the
+// read is in flight).
+__device__ __forceinline__ u32x2_t ds_read_tr16_b64(uint32_t lds_addr) {
+  u32x2_t r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(lds_addr));
+  return r;
+}
+// Wait for this wavefront's outstanding LDS operations (lgkmcnt = 0).
+__device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// Orders the uses of v after the preceding lds_wait() (emits nothing).
+__device__ __forceinline__ void lds_hold(u32x2_t& v) { asm volatile("" : "+v"(v)); }
+
 // GELU u * Phi(u) = u/2 * (1 + erf(u / sqrt 2)) and its derivative
 // Phi(u) + u * phi(u).  erfc(|u| / sqrt 2) is evaluated with the rational
 // approximation of Abramowitz & Stegun, Handbook of Mathematical Functions,

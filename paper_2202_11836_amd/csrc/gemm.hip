@@ -181,7 +181,21 @@ __device__ __forceinline__ void dma_tile(__amdgpu_buffer_rsrc_t rs, int64_t ld, 
 // k-row k0 + j / 4, columns mb + 4 (j % 4), so lane i receives column mb + i
 // at k-rows k0 .. k0 + 3 (the second read: k0 + 4 .. k0 + 7).
 typedef __attribute__((address_space(3))) char lds_char_t;
-typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+
+// An m/n-major fragment as read: the two halves of the transposing reads
+// (ds_read_tr16_b64), combined only after lds_wait() / frag_hold().
+struct TrFrag {
+  u32x2_t lo, hi;
+};
+__device__ __forceinline__ bf16x8_t frag_val(const bf16x8_t& v) { return v; }
+__device__ __forceinline__ bf16x8_t frag_val(const TrFrag& v) {
+  return __builtin_bit_cast(bf16x8_t, u32x4_t{v.lo[0], v.lo[1], v.hi[0], v.hi[1]});
+}
+__device__ __forceinline__ void frag_hold(bf16x8_t&) {}
+__device__ __forceinline__ void frag_hold(TrFrag& v) {
+  lds_hold(v.lo);
+  lds_hold(v.hi);
+}
 
 // Per-lane LDS addresses of one operand's fragments in ring slot 0, so that
 // every fragment read in the main loop is one instruction with an immediate
@@ -194,6 +208,7 @@ template <int R, bool KMAJ, int BK, int NF>
 struct FragPtrs {
   static constexpr int KS = BK / 16;
   static constexpr int N = KMAJ ? KS : NF;
+  using Frag = typename std::conditional<KMAJ, bf16x8_t, TrFrag>::type;
   uint32_t p[N];
   __device__ __forceinline__ void init(uint32_t base, int r0, int lane) {
     if constexpr (KMAJ) {
@@ -216,17 +231,13 @@ struct FragPtrs {
     for (int n = 0; n < N; ++n) p[n] += delta;
   }
   // fragment f of k-step ks
-  __device__ __forceinline__ bf16x8_t get(int f, int ks) const {
+  __device__ __forceinline__ Frag get(int f, int ks) const {
     if constexpr (KMAJ) {
       return *(const __attribute__((address_space(3))) bf16x8_t*)(
           (const lds_char_t*)(uintptr_t)p[ks] + f * 32 * (2 * BK));
     } else {
-      const lds_char_t* q = (const lds_char_t*)(uintptr_t)p[f] + ks * 16 * (2 * R);
-      const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-          (__attribute__((address_space(3))) bf16x4_t*)(q));
-      const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-          (__attribute__((address_space(3))) bf16x4_t*)(q + 4 * (2 * R)));
-      return bf16x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      const uint32_t q = p[f] + ks * 16 * (2 * R);
+      return TrFrag{ds_read_tr16_b64(q), ds_read_tr16_b64(q + 4 * (2 * R))};
     }
   }
 };
@@ -581,6 +592,9 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
   const int wm = wave / C::WGN, wn = wave % C::WGN;
   const int hf = lane >> 5, rr = lane & 31;
   constexpr int KS = C::BK / 16;
+  // Transposing fragment reads (an m/n-major operand): issued as inline
+  // assembly, waited for explicitly.
+  constexpr bool TR = !AK || !BKM;
 
   // First k-tiles of the first output tile.
 #pragma unroll
@@ -599,9 +613,12 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
 
     // The first k-tiles are in flight (issued before the previous epilogue
     // or above); wait for everything outstanding, then read k-tile 0.
-    bf16x8_t af[2][TM], bfr[2][TN];
-    FragPtrs<BM, AK, C::BK, TM> pa;
-    FragPtrs<BN, BKM, C::BK, TN> pb;
+    using PA = FragPtrs<BM, AK, C::BK, TM>;
+    using PB = FragPtrs<BN, BKM, C::BK, TN>;
+    typename PA::Frag af[2][TM];
+    typename PB::Frag bfr[2][TN];
+    PA pa;
+    PB pb;
     const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_char_t*)smem;
     pa.init(lds0, wm * C::WM, lane);
     pb.init(lds0 + C::A_BYTES, wn * C::WN, lane);
@@ -650,11 +667,24 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         const int cur = ks & 1, nxt = cur ^ 1;
+        if constexpr (TR) {
+          // This k-step's fragments (read during the previous one) have
+          // landed; the transposing reads are not tracked by the compiler.
+          lds_wait();
+#pragma unroll
+          for (int i = 0; i < TM; ++i) frag_hold(af[cur][i]);
+#pragma unroll
+          for (int j = 0; j < TN; ++j) frag_hold(bfr[cur][j]);
+        }
         if (ks + 1 < KS) {
+          if constexpr (TR) {
+            // Interleaved below, with the MFMAs.
+          } else {
 #pragma unroll
           for (int i = 0; i < TM; ++i) af[nxt][i] = pa.get(i, ks + 1);
 #pragma unroll
           for (int j = 0; j < TN; ++j) bfr[nxt][j] = pb.get(j, ks + 1);
+          }
         } else {
           // Unconditional (also for the last k-tile, whose "next" fragments
           // are never used): a branch here would make the compiler wait for
@@ -666,11 +696,33 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
           const int delta = ((t + 1) % NS == 0) ? -(NS - 1) * C::STAGE_BYTES : C::STAGE_BYTES;
           pa.advance(delta);
           pb.advance(delta);
+          if constexpr (!TR) {
 #pragma unroll
-          for (int i = 0; i < TM; ++i) af[nxt][i] = pa.get(i, 0);
+            for (int i = 0; i < TM; ++i) af[nxt][i] = pa.get(i, 0);
 #pragma unroll
-          for (int j = 0; j < TN; ++j) bfr[nxt][j] = pb.get(j, 0);
+            for (int j = 0; j < TN; ++j) bfr[nxt][j] = pb.get(j, 0);
+          }
         }
+        if constexpr (TR) {
+          // One MFMA, then its share of the next k-step's fragment reads
+          // (from the next k-tile after the last k-step), in this order:
+          // each read issues while the matrix core works on the MFMA
+          // before it.
+          constexpr int NM = TM * TN, NF = TM + TN;
+          const int kn = ks + 1 < KS ? ks + 1 : 0;
+#pragma unroll
+          for (int m = 0; m < NM; ++m) {
+            acc[m / TN][m % TN] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                frag_val(af[cur][m / TN]), frag_val(bfr[cur][m % TN]), acc[m / TN][m % TN], 0, 0, 0);
+#pragma unroll
+            for (int f = 0; f < NF; ++f)
+              if ((f * NM) / NF == m) {
+                if (f < TM) af[nxt][f] = pa.get(f, kn);
+                else bfr[nxt][f - TM] = pb.get(f - TM, kn);
+              }
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        } else {
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -691,8 +743,18 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
             __builtin_amdgcn_sched_group_barrier(0x100, (NR + NM - 1) / NM, 0);  // LDS read
           }
         }
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
+    }
+    if constexpr (TR) {
+      // The last k-step's reads of the "next" fragments (never used) must
+      // land before their registers are reused.
+      lds_wait();
+#pragma unroll
+      for (int i = 0; i < TM; ++i) frag_hold(af[0][i]), frag_hold(af[1][i]);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) frag_hold(bfr[0][j]), frag_hold(bfr[1][j]);
     }
 
     // Every wavefront has read its last fragments: the whole ring is free.
