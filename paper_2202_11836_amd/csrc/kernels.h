@@ -139,22 +139,6 @@ hipError_t ln_bwd_bf16(const bf16_t* dy, const bf16_t* ahi, const bf16_t* alo, c
 hipError_t add3_bf16(const bf16_t* ahi, const bf16_t* alo, const bf16_t* b, bf16_t* out,
                      int64_t n, hipStream_t st);
 
-// dst[c][r] = src[r][c] for a bf16 [R][C] matrix.
-// dst[c][r] = src[r][c] for up to TRANSPOSE_MAX_JOBS row-major R x C bf16
-// matrices in one launch (R, C multiples of 8; tile0 is filled in).
-constexpr int TRANSPOSE_MAX_JOBS = 8;
-struct TransposeJob {
-  const bf16_t* src;
-  bf16_t* dst;
-  int R, C;
-  int tile0;
-};
-struct TransposeBatch {
-  TransposeJob job[TRANSPOSE_MAX_JOBS];
-  int n;
-};
-hipError_t transpose_bf16(const TransposeJob* jobs, int n, hipStream_t st);
-
 // part[blk][n] = sum over the block's rows of x[row][n].
 template <typename T>
 hipError_t col_partial(const T* x, int rows, int n, float* part, int nblk, hipStream_t st);

@@ -483,64 +483,7 @@ __global__ __launch_bounds__(256) void softmax_bwd_kernel(const float* __restric
   }
 }
 
-// Batched bf16 transpose dst[c][r] = src[r][c] over 64 x 64 tiles; rows and
-// columns are multiples of 8 so HBM is read and written in 16-byte pieces.
-// Work-group b handles tile b - job.tile0 of the job whose range holds b.
-__global__ __launch_bounds__(256) void transpose_bf16_kernel(TransposeBatch jb) {
-  // 16-byte chunk c of tile row r sits at chunk c ^ ((r >> 3) & 7): the
-  // column reads below (8 rows r = 8 ch + .. per lane, one column per lane)
-  // then hit 32 distinct banks per wavefront.
-  __shared__ __attribute__((aligned(16))) bf16_t t[64][64];
-  int k = 0;
-  while (k + 1 < jb.n && (int)blockIdx.x >= jb.job[k + 1].tile0) ++k;
-  const TransposeJob J = jb.job[k];
-  const int tiles_c = (J.C + 63) / 64;
-  const int tile = blockIdx.x - J.tile0;
-  const int r0 = (tile / tiles_c) * 64, c0 = (tile % tiles_c) * 64;
-#pragma unroll
-  for (int p = 0; p < 2; ++p) {
-    const int idx = threadIdx.x + 256 * p;
-    const int row = idx >> 3, ch = idx & 7;
-    const int r = r0 + row, c = c0 + 8 * ch;
-    u32x4_t v = {0, 0, 0, 0};
-    if (r < J.R && c < J.C) v = *(const u32x4_t*)(J.src + (int64_t)r * J.C + c);
-    *(u32x4_t*)&t[row][8 * (ch ^ ((row >> 3) & 7))] = v;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int p = 0; p < 2; ++p) {
-    const int idx = threadIdx.x + 256 * p;
-    const int orow = idx >> 3, ch = idx & 7;  // output row = source column c0 + orow
-    const int c = c0 + orow, r = r0 + 8 * ch;
-    if (c < J.C && r < J.R) {
-      u32x4_t o;
-      const int pc = 8 * ((orow >> 3) ^ ch) + (orow & 7);  // rows 8 ch .. 8 ch + 7
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        o[e] = (uint32_t)t[8 * ch + 2 * e][pc] | ((uint32_t)t[8 * ch + 2 * e + 1][pc] << 16);
-      *(u32x4_t*)(J.dst + (int64_t)c * J.R + r) = o;
-    }
-  }
-}
-
 }  // namespace
-
-hipError_t transpose_bf16(const TransposeJob* jobs, int n, hipStream_t st) {
-  TransposeBatch b;
-  int tiles = 0;
-  b.n = 0;
-  for (int k = 0; k < n; ++k) {
-    if (jobs[k].R <= 0 || jobs[k].C <= 0) continue;
-    if (jobs[k].R % 8 || jobs[k].C % 8 || b.n == TRANSPOSE_MAX_JOBS) return hipErrorInvalidValue;
-    b.job[b.n] = jobs[k];
-    b.job[b.n].tile0 = tiles;
-    tiles += ((jobs[k].R + 63) / 64) * ((jobs[k].C + 63) / 64);
-    ++b.n;
-  }
-  if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL(transpose_bf16_kernel, dim3(tiles), dim3(256), 0, st, b);
-  return hipGetLastError();
-}
 
 template <typename T, typename TA>
 hipError_t add_ln_fwd(const TA* a, const float* bias, const T* resid, const T* resid_lo,

@@ -40,7 +40,7 @@ constexpr int COL_PARTS = 128; // row blocks of the bias-gradient column sums
   X(BQKV_RED, "bqkv_colreduce") X(WQKV_WGRAD, "wqkv_wgrad_gemm")                        \
   X(WQKV_RED, "wqkv_wgrad_splitk_reduce") X(QKV_DGRAD, "qkv_dgrad_resid_gemm")            \
   X(KEXT, "key_extent") X(ATTN_FWD, "attn_fwd") X(ATTN_DQ, "attn_bwd_dq")                 \
-  X(ATTN_DKDV, "attn_bwd_dkdv") X(WT, "weight_transpose")                                \
+  X(ATTN_DKDV, "attn_bwd_dkdv")                                \
   X(WGRAD_GROUP, "wgrad_group_gemm") X(WGRAD_GROUP_RED, "wgrad_group_splitk_reduce")
 
 enum Site {
@@ -181,10 +181,6 @@ struct stage {
   float* colpart_qkv = nullptr;  // [B * ceil(S/32), 3h] column sums of dQKV (bf16 stages)
   // Transposed weights of the layer being differentiated (bf16 stages), so
   // that every data-gradient GEMM reads both operands k-contiguously.
-  void* wt_qkv = nullptr;   // [h, 3h]
-  void* wt_o = nullptr;     // [h, h]
-  void* wt_1 = nullptr;     // [h, f]
-  void* wt_2 = nullptr;     // [f, h]
   float* splitk = nullptr;  // split-K partials of the weight gradients
   size_t splitk_elems = 0;  // elements it holds
   size_t splitk_bytes = 0;  // bytes counted for it in bytes_act
@@ -464,9 +460,6 @@ stage_status ensure_activations(stage_t* s, int B, int S) {
   const int64_t nqb = ((int64_t)S + 31) / 32;
   if ((st = A((void**)&s->colpart_ffn, ((T + 127) / 128) * f * 4)) ||
       (st = A((void**)&s->colpart_qkv, (int64_t)B * nqb * 3 * h * 4)))
-    return st;
-  if ((st = A(&s->wt_qkv, 3 * h * h * e)) || (st = A(&s->wt_o, h * h * e)) ||
-      (st = A(&s->wt_1, f * h * e)) || (st = A(&s->wt_2, h * f * e)))
     return st;
   const int64_t maxw = std::max<int64_t>(3 * h, f);
   const int64_t part_elems =
@@ -881,9 +874,9 @@ struct GradIn {
 // Backward of a bf16 stage.  Per layer: the LayerNorm backward kernels take
 // GradIn and write dZ in bf16 (GEMM operand) and fp32 (residual branch);
 // the two data-gradient GEMMs whose output feeds a residual addition store
-// their product in fp32 (the addition happens in the next LayerNorm
-// backward); the weights are transposed once so that every data-gradient
-// GEMM reads both operands k-contiguously; the four weight gradients and
+// their product in bf16 (the addition happens in the next LayerNorm
+// backward); the data-gradient GEMMs read the weights as stored (n-major B
+// operand, transposing LDS reads); the four weight gradients and
 // the bias / LayerNorm column reductions run in one group launch and one
 // reduction launch at the end of the layer.
 stage_status backward_bf16(stage_t* s, const bf16_t* dy, bf16_t* dx) {
@@ -908,19 +901,6 @@ stage_status backward_bf16(stage_t* s, const bf16_t* dy, bf16_t* dx) {
     int nw = 0;
     ColJob cjobs[COLJOB_MAX];
     int nc = 0;
-    {
-      TransposeJob jobs[4];
-      int nj = 0;
-      if (attn) {
-        jobs[nj++] = {(const T*)p[STAGE_W_QKV], (T*)s->wt_qkv, 3 * h, h, 0};
-        jobs[nj++] = {(const T*)p[STAGE_W_O], (T*)s->wt_o, h, h, 0};
-      }
-      if (ffn) {
-        jobs[nj++] = {(const T*)p[STAGE_W_1], (T*)s->wt_1, f, h, 0};
-        jobs[nj++] = {(const T*)p[STAGE_W_2], (T*)s->wt_2, h, f, 0};
-      }
-      SITE(WT, transpose_bf16(jobs, nj, st));
-    }
     // Gradient reaching H1: from the feed-forward half, or the incoming dy
     // when the stage ends at this layer's attention half.
     GradIn gh1 = gin;
@@ -935,12 +915,12 @@ stage_status backward_bf16(stage_t* s, const bf16_t* dy, bf16_t* dx) {
       wjobs[nw++] = {dZ2, h, v.G, f, h, f, gr[STAGE_W_2]};
       // dU = (dZ2 W_2) * GELU'(U); db_1 = column sums of dU (epilogue)
       {
-        GemmArgs g = gemm_args(dZ2, h, s->wt_2, h, dU, f, Tn, f, h);
+        GemmArgs g = gemm_args(dZ2, h, p[STAGE_W_2], f, dU, f, Tn, f, h);
         g.aux = v.Gd;
         g.ldaux = f;
         g.tile = 1;
         g.colpart = s->colpart_ffn;
-        SITE(FFN2_DGRAD, gemm_bf16(g, true, true, EPI_MUL, false, 1, st));
+        SITE(FFN2_DGRAD, gemm_bf16(g, true, false, EPI_MUL, false, 1, st));
       }
       cjobs[nc++] = ColJob{s->colpart_ffn, (Tn + 127) / 128, 1, f,
                            {gr[STAGE_B_1], nullptr, nullptr, nullptr}};
@@ -950,8 +930,8 @@ stage_status backward_bf16(stage_t* s, const bf16_t* dy, bf16_t* dx) {
       // LayerNorm's backward (or here, rounded, when this half is the
       // stage's first unit and dH1 is its dx)
       {
-        GemmArgs g = gemm_args(dU, f, s->wt_1, f, s->prod, h, Tn, h, f);
-        SITE(FFN1_DGRAD, gemm_bf16(g, true, true, EPI_STORE, false, 1, st));
+        GemmArgs g = gemm_args(dU, f, p[STAGE_W_1], h, s->prod, h, Tn, h, f);
+        SITE(FFN1_DGRAD, gemm_bf16(g, true, false, EPI_STORE, false, 1, st));
       }
       if (attn) {
         gh1 = GradIn{nullptr, dZ2, (const T*)s->dz2lo, (const T*)s->prod};
@@ -970,8 +950,8 @@ stage_status backward_bf16(stage_t* s, const bf16_t* dy, bf16_t* dx) {
       wjobs[nw++] = {dZ1, h, v.C, h, h, h, gr[STAGE_W_O]};
       // dC = dZ1 W_o
       {
-        GemmArgs g = gemm_args(dZ1, h, s->wt_o, h, dC, h, Tn, h, h);
-        SITE(OUT_DGRAD, gemm_bf16(g, true, true, EPI_STORE, false, 1, st));
+        GemmArgs g = gemm_args(dZ1, h, p[STAGE_W_O], h, dC, h, Tn, h, h);
+        SITE(OUT_DGRAD, gemm_bf16(g, true, false, EPI_STORE, false, 1, st));
       }
       // Attention backward (recomputes P from the saved log-sum-exp): dQKV
       // and the column sums of db_qkv per 32-row block.
@@ -989,8 +969,8 @@ stage_status backward_bf16(stage_t* s, const bf16_t* dy, bf16_t* dx) {
       // dX = dZ1 + dQKV W_qkv: the product in bf16; the sum in the previous
       // layer's second LayerNorm backward, or here, rounded, for the stage's dx
       {
-        GemmArgs g = gemm_args(dQKV, 3 * h, s->wt_qkv, 3 * h, s->prod, h, Tn, h, 3 * h);
-        SITE(QKV_DGRAD, gemm_bf16(g, true, true, EPI_STORE, false, 1, st));
+        GemmArgs g = gemm_args(dQKV, 3 * h, p[STAGE_W_QKV], h, s->prod, h, Tn, h, 3 * h);
+        SITE(QKV_DGRAD, gemm_bf16(g, true, false, EPI_STORE, false, 1, st));
       }
       if (l > 0) {
         gin = GradIn{nullptr, dZ1, (const T*)s->dz1lo, (const T*)s->prod};
