@@ -140,7 +140,7 @@ def depth_sweep(cfg, depths, steps, warmup):
             st.forward(x, mask, out=y)
             st.backward(dy, out=dx)
         torch.cuda.synchronize()
-        fwd = bwd = 0.0
+        fs, bs = [], []
         for _ in range(steps):
             ev[0].record()
             st.forward(x, mask, out=y)
@@ -148,9 +148,11 @@ def depth_sweep(cfg, depths, steps, warmup):
             st.backward(dy, out=dx)
             ev[2].record()
             torch.cuda.synchronize()
-            fwd += ev[0].elapsed_time(ev[1]) / steps
-            bwd += ev[1].elapsed_time(ev[2]) / steps
+            fs.append(ev[0].elapsed_time(ev[1]))
+            bs.append(ev[1].elapsed_time(ev[2]))
         st.close()
+        # medians over the steps (a step's fwd and bwd from the same events)
+        fwd, bwd = float(np.median(fs)), float(np.median(bs))
         rows.append({"L": L, "fwd_ms": fwd, "bwd_ms": bwd, "step_ms": fwd + bwd,
                      "per_layer_ms": (fwd + bwd) / L})
         print(f"L={L:3d}  step {fwd + bwd:8.3f} ms  per layer {(fwd + bwd) / L:7.3f} ms",
@@ -169,6 +171,7 @@ def depth_sweep(cfg, depths, steps, warmup):
         "data": "synthetic (seeded N(0,1) inputs, N(0,0.02) weights)",
         "steps": steps,
         "warmup": warmup,
+        "timing": "fwd_ms, bwd_ms: medians over the steps of HIP events on the stage stream",
         "config": {"workload": f"{cfg.name}: h{cfg.hidden}, {cfg.heads} heads, ffn {cfg.ffn}, "
                                f"B{cfg.batch} x S{cfg.seq}, valid lengths in "
                                f"[{cfg.len_lo},{cfg.len_hi}]"},

@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 typedef uint16_t bf16_t;  // bfloat16 storage (upper half of an fp32)
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -59,10 +61,23 @@ __device__ __forceinline__ float wave_max(float v) {
 // result must pass lds_wait() and then lds_hold() before any use, and must
 // stay live until then (its register could otherwise be reused while the
 // read is in flight).
+// OFF: a constant byte offset, carried in the instruction's offset field.
+template <int OFF = 0>
 __device__ __forceinline__ u32x2_t ds_read_tr16_b64(uint32_t lds_addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "LDS instruction offset range");
   u32x2_t r;
-  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(lds_addr));
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(lds_addr), "i"(OFF));
   return r;
+}
+
+// f(std::integral_constant<int, I>()) for I = B .. E - 1: a loop whose index
+// is a constant expression in the body.
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>());
+    static_for<B + 1, E>(f);
+  }
 }
 // Wait for this wavefront's outstanding LDS operations (lgkmcnt = 0).
 __device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }

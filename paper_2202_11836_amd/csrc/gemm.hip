@@ -230,14 +230,15 @@ struct FragPtrs {
 #pragma unroll
     for (int n = 0; n < N; ++n) p[n] += delta;
   }
-  // fragment f of k-step ks
-  __device__ __forceinline__ Frag get(int f, int ks) const {
+  // fragment f of k-step KSI
+  template <int KSI>
+  __device__ __forceinline__ Frag get(int f) const {
     if constexpr (KMAJ) {
       return *(const __attribute__((address_space(3))) bf16x8_t*)(
-          (const lds_char_t*)(uintptr_t)p[ks] + f * 32 * (2 * BK));
+          (const lds_char_t*)(uintptr_t)p[KSI] + f * 32 * (2 * BK));
     } else {
-      const uint32_t q = p[f] + ks * 16 * (2 * R);
-      return TrFrag{ds_read_tr16_b64(q), ds_read_tr16_b64(q + 4 * (2 * R))};
+      return TrFrag{ds_read_tr16_b64<KSI * 16 * (2 * R)>(p[f]),
+                    ds_read_tr16_b64<KSI * 16 * (2 * R) + 4 * (2 * R)>(p[f])};
     }
   }
 };
@@ -653,9 +654,9 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
     __syncthreads();
     if (ntiles > 0) {
 #pragma unroll
-      for (int i = 0; i < TM; ++i) af[0][i] = pa.get(i, 0);
+      for (int i = 0; i < TM; ++i) af[0][i] = pa.template get<0>(i);
 #pragma unroll
-      for (int j = 0; j < TN; ++j) bfr[0][j] = pb.get(j, 0);
+      for (int j = 0; j < TN; ++j) bfr[0][j] = pb.template get<0>(j);
     }
     // Main loop.  While the MFMAs of k-step ks run, the fragments of ks + 1
     // are read; in the last k-step of a k-tile they come from the next
@@ -664,9 +665,9 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
     // landed and nobody reads k-tile t's slot any more), refill that slot
     // with k-tile t + NS, then read.
     for (int t = 0; t < ntiles; ++t) {
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const int cur = ks & 1, nxt = cur ^ 1;
+      static_for<0, KS>([&](auto ksc) {
+        constexpr int ks = decltype(ksc)::value;
+        constexpr int cur = ks & 1, nxt = cur ^ 1;
         if constexpr (TR) {
           // This k-step's fragments (read during the previous one) have
           // landed; the transposing reads are not tracked by the compiler.
@@ -681,9 +682,9 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
             // Interleaved below, with the MFMAs.
           } else {
 #pragma unroll
-          for (int i = 0; i < TM; ++i) af[nxt][i] = pa.get(i, ks + 1);
+          for (int i = 0; i < TM; ++i) af[nxt][i] = pa.template get<(ks + 1) % KS>(i);
 #pragma unroll
-          for (int j = 0; j < TN; ++j) bfr[nxt][j] = pb.get(j, ks + 1);
+          for (int j = 0; j < TN; ++j) bfr[nxt][j] = pb.template get<(ks + 1) % KS>(j);
           }
         } else {
           // Unconditional (also for the last k-tile, whose "next" fragments
@@ -698,9 +699,9 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
           pb.advance(delta);
           if constexpr (!TR) {
 #pragma unroll
-            for (int i = 0; i < TM; ++i) af[nxt][i] = pa.get(i, 0);
+            for (int i = 0; i < TM; ++i) af[nxt][i] = pa.template get<0>(i);
 #pragma unroll
-            for (int j = 0; j < TN; ++j) bfr[nxt][j] = pb.get(j, 0);
+            for (int j = 0; j < TN; ++j) bfr[nxt][j] = pb.template get<0>(j);
           }
         }
         if constexpr (TR) {
@@ -709,7 +710,7 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
           // each read issues while the matrix core works on the MFMA
           // before it.
           constexpr int NM = TM * TN, NF = TM + TN;
-          const int kn = ks + 1 < KS ? ks + 1 : 0;
+          constexpr int kn = ks + 1 < KS ? ks + 1 : 0;
 #pragma unroll
           for (int m = 0; m < NM; ++m) {
             acc[m / TN][m % TN] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
@@ -717,8 +718,8 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
 #pragma unroll
             for (int f = 0; f < NF; ++f)
               if ((f * NM) / NF == m) {
-                if (f < TM) af[nxt][f] = pa.get(f, kn);
-                else bfr[nxt][f - TM] = pb.get(f - TM, kn);
+                if (f < TM) af[nxt][f] = pa.template get<kn>(f);
+                else bfr[nxt][f - TM] = pb.template get<kn>(f - TM);
               }
             __builtin_amdgcn_sched_barrier(0);
           }
@@ -745,7 +746,7 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
         }
         }
         __builtin_amdgcn_sched_barrier(0);
-      }
+      });
     }
     if constexpr (TR) {
       // The last k-step's reads of the "next" fragments (never used) must
