@@ -110,6 +110,10 @@ struct TileCfg {
   static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
   // direct-to-LDS load instructions per k-tile per wavefront (1 KB each)
   static constexpr int DMA_PER_TILE = STAGE_BYTES / 1024 / WAVES;
+  // Requests of a k-tile split in time over the work-group (see the main
+  // loop): on for the 2- and 3-slot rings, off for the 4-slot one (128 x 128
+  // tiles), where it measured slower.
+  static constexpr bool STAGGER = NS <= 3;
   // Epilogue staging, beside the ring: 16 rows x WN fp32 per wavefront.
   static constexpr int EPI_BYTES = WAVES * 16 * WN * 4;
   static constexpr int LDS_BYTES = NS * STAGE_BYTES + EPI_BYTES;
@@ -664,10 +668,31 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
     // its reads of k-tile t, barrier (every wavefront's k-tile t + 1 has
     // landed and nobody reads k-tile t's slot any more), refill that slot
     // with k-tile t + NS, then read.
+    //
+    // With STAGGER only the first half of the wavefronts (0 .. WAVES/2 - 1)
+    // request their part of k-tile t + NS right after that barrier; the
+    // other half request theirs at the start of k-tile t + 1.  Issuing the
+    // direct-to-LDS loads stalls a wavefront until the CU's address unit
+    // takes them (64 KB per k-tile for 256 x 256), and wavefronts w and
+    // w + 4 share a SIMD: split this way, one of each pair issues MFMAs
+    // while the other issues its loads, instead of both stalling at once.
+    // The slot is free for both halves: its last reads (k-tile t) completed
+    // before the barrier.  Before the wait at the end of any k-tile both
+    // halves have requested the same k-tiles, so that wait is unchanged.
+    // Measured (same box): 256 x 256 encoder GEMM set -3.9%, weight-
+    // gradient group -5%, 8192^3 -3%, 256 x 128 tiles at 4096 tokens -2% to
+    // -11% (128 x 128: +1% to +7%, hence off there); splitting the pairs the other way
+    // (even / odd wavefronts) or each wavefront's own loads in two gave
+    // -0.3% to -1.6%; requesting the second half one or two k-steps later
+    // was slower than not splitting.
     for (int t = 0; t < ntiles; ++t) {
       static_for<0, KS>([&](auto ksc) {
         constexpr int ks = decltype(ksc)::value;
         constexpr int cur = ks & 1, nxt = cur ^ 1;
+        if constexpr (C::STAGGER && ks == 0) {
+          if (wave >= C::WAVES / 2 && t >= 1 && t - 1 + NS < ntiles)
+            issue_ktile<BM, BN, AK, BKM>(g, T, t - 1 + NS, smem, wave, lane);
+        }
         if constexpr (TR) {
           // This k-step's fragments (read during the previous one) have
           // landed; the transposing reads are not tracked by the compiler.
@@ -692,7 +717,8 @@ __global__ __launch_bounds__((64 * RingShape<BM, BN>::WAVES), 1) void gemm_bf16_
           // these reads before the last k-step's MFMAs.
           wait_ktile<C::DMA_PER_TILE, NS>(min(ntiles - 1, t + NS - 1) - (t + 1));
           __syncthreads();
-          if (t + NS < ntiles) issue_ktile<BM, BN, AK, BKM>(g, T, t + NS, smem, wave, lane);
+          if (t + NS < ntiles && !(C::STAGGER && wave >= C::WAVES / 2))
+            issue_ktile<BM, BN, AK, BKM>(g, T, t + NS, smem, wave, lane);
           // move the fragment pointers to the next ring slot
           const int delta = ((t + 1) % NS == 0) ? -(NS - 1) * C::STAGE_BYTES : C::STAGE_BYTES;
           pa.advance(delta);
