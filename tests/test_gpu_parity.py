@@ -267,6 +267,29 @@ def test_bf16_bert_base_8_uneven_sequence_subset():
     assert_bf16(lw, check_bf16(cfg, got, ref, rows=sel))
 
 
+def test_bf16_mid_width_sequence_subset():
+    """Two layers of width 512 (8 heads, FFN 2048) on B32 x S512 with valid
+    lengths in [384, 512].  On a 256-CU device the GEMMs with N = h = 512
+    (out-projection, FFN2, the FFN1 / QKV / out-projection data gradients)
+    take 256 x 128 tiles, the three-slot ring with its k-tile requests split
+    between the two halves of the work-group, which none of the other
+    configurations selects.  dy is zero outside three sequences (the first,
+    the shortest and the last); the oracle runs only those."""
+    cfg = synth.StageConfig("mid_width", 2, 512, 8, 2048, 32, 512, 384, 512, "bf16", 7)
+    _say(f"case bf16 subset {cfg}")
+    inp = synth.make_inputs(cfg)
+    params = synth.make_params(cfg)
+    sel = np.zeros(cfg.batch, bool)
+    sel[[0, int(np.argmin(inp["lengths"])), cfg.batch - 1]] = True
+    dy = inp["dy"].copy()
+    dy[~sel] = 0.0
+    got = run_gpu(cfg, inp, params, dy=dy, saved=(0, 3))
+    lw = check_bf16_layerwise(cfg, inp, params, got, seqs=np.flatnonzero(sel))
+    sub = {"x": inp["x"][sel], "mask": inp["mask"][sel], "dy": dy[sel]}
+    ref = run_oracle(cfg.with_(batch=int(sel.sum())), sub, params)
+    assert_bf16(lw, check_bf16(cfg, got, ref, rows=sel))
+
+
 def test_bf16_smaller_batches_after_the_full_batch():
     """One BERT-large-shaped layer run on B32 x S512 and then, on the same
     stage, on smaller batches.  The weight-gradient stream-K schedule of a
