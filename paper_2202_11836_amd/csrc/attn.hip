@@ -258,13 +258,35 @@ __device__ __forceinline__ void store_kfull(int* flags, float bias, int lane) {
   }
 }
 
+// A kernel's LDS is one object.  With several __shared__ variables the
+// compiler tags each access with the variable's alias scope and then makes
+// the first LDS read after a direct-to-LDS load wait for that load
+// (vmcnt(0)), although the read is of the other stage: the next block's
+// loads then completed before the current block's first MFMA instead of
+// under its work.  With a single object it does not for the 16-byte
+// fragment reads (measured in the assembly); the transposing-read builtin
+// still waits, at the first sub-block's second product.  The kernels' own
+// waits (wait_all and the barrier at each block) order every read after the
+// loads it depends on.  Same harness and box, medians of three: forward
+// -1.6%, dQ -2.7%, dQ then dK/dV -3.2% (with the set-up and per-block load
+// order below; reading the transposed fragments as inline assembly to avoid
+// the builtin's wait was slower).
+struct LdsKV {
+  char tiles[2][2 * TILE];  // per stage: K, V
+  float kbias[2][KT];       // per stage: 0 or -inf per key
+  int kfull[2][2];          // per stage and 32-key half: no key masked
+};
+
 // ---------------------------------------------------------------------------
 // Forward: wavefront = 32 queries; block = 128 queries of one (batch, head).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(1024))) char tiles[2][2 * TILE];  // per stage: K, V
-  __shared__ __attribute__((aligned(16))) float kbias[2][KT];         // 0 or -inf per key
-  __shared__ int kfull[2][2];  // per stage and 32-key half: no key masked
+  // One LDS object (see LdsKV): K, V per stage; key bias 0 or -inf per key;
+  // per stage and 32-key half, whether no key is masked.
+  __shared__ __attribute__((aligned(1024))) LdsKV lds;
+  auto& tiles = lds.tiles;
+  auto& kbias = lds.kbias;
+  auto& kfull = lds.kfull;
 
   int qb, bh;
   attn_block((a.S + 127) / 128, qb, bh);
@@ -280,20 +302,22 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
   const int kend = a.kext[b];
   const int nkb = (kend + KT - 1) / KT;
   const __amdgpu_buffer_rsrc_t rsK = rows_rsrc(Kg, S, ld), rsV = rows_rsrc(Vg, S, ld);
-  auto bias_of = [&](int kb) {
-    const int k = kb * KT + tid;
-    return (k < kend && mrow[k] != 0) ? 0.0f : -INFINITY;
+  // Mask byte of key kb KT + tid (clamped to a valid key, so that the load
+  // is unconditional) and the key bias it gives (0 or -inf).  Wavefront 0
+  // loads the bytes of block kb + 2 during block kb and turns them into the
+  // bias of block kb + 2 at the end of block kb + 1, after the wait at that
+  // block's start: using them in the block that loads them made it wait a
+  // memory latency per block, and the other wavefronts then waited for it at
+  // the next barrier.
+  auto mask_raw = [&](int kb) { return (int)mrow[min(kb * KT + tid, S - 1)]; };
+  auto bias_from = [&](int kb, int raw) {
+    return (kb * KT + tid < kend && raw != 0) ? 0.0f : -INFINITY;
   };
+  auto bias_of = [&](int kb) { return bias_from(kb, mask_raw(kb)); };
 
-  if (nkb > 0) {
-    if (tid < KT) {  // wavefront 0
-      const float kb0 = bias_of(0);
-      kbias[0][tid] = kb0;
-      store_kfull(kfull[0], kb0, tid);
-    }
-    dma_rows(rsK, 0, ld, tiles[0], wave, lane);
-    dma_rows(rsV, 0, ld, tiles[0] + TILE, wave, lane);
-  }
+  // Set-up loads in the order that lets their latencies overlap: the
+  // wavefront's own operand fragments, the first streamed block, and only
+  // then the key-mask bytes, whose values the LDS set-up waits for.
   // Q^T as the B operand: lane = query q0 + rr, dims 16 ks + 8 hf .. +7.
   bf16x8_t qf[4];
   {
@@ -303,6 +327,16 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
       qf[ks] = q < S ? ld_frag(Qg + (int64_t)q * ld + 16 * ks + 8 * hf)
                      : __builtin_bit_cast(bf16x8_t, zero4());
   }
+  if (nkb > 0) {
+    dma_rows(rsK, 0, ld, tiles[0], wave, lane);
+    dma_rows(rsV, 0, ld, tiles[0] + TILE, wave, lane);
+    if (tid < KT) {  // wavefront 0
+      const float kb0 = bias_of(0);
+      kbias[0][tid] = kb0;
+      store_kfull(kfull[0], kb0, tid);
+    }
+  }
+  int nraw = (tid < KT && nkb > 1) ? mask_raw(1) : 0;  // bytes of the next block
   float m = -INFINITY, lsum = 0.0f;  // exponent offset (log2 units) and partial sum
   f32x16_t acc[2] = {zero16(), zero16()};  // O^T: dims 0-31, 32-63 x queries
 
@@ -312,12 +346,11 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
     // barrier for everyone's) and nobody reads the other stage any more.
     wait_all();
     __syncthreads();
-    float nbias = 0.0f;
     if (kb + 1 < nkb) {
-      if (tid < KT) nbias = bias_of(kb + 1);
       dma_rows(rsK, (kb + 1) * KT, ld, tiles[st ^ 1], wave, lane);
       dma_rows(rsV, (kb + 1) * KT, ld, tiles[st ^ 1] + TILE, wave, lane);
     }
+    const int nraw2 = (tid < KT && kb + 2 < nkb) ? mask_raw(kb + 2) : 0;
     const char* Ks = tiles[st];
     const char* Vs = tiles[st] + TILE;
 #pragma unroll
@@ -390,9 +423,11 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
       }
     }
     if (kb + 1 < nkb && tid < KT) {
+      const float nbias = bias_from(kb + 1, nraw);
       kbias[st ^ 1][tid] = nbias;
       store_kfull(kfull[st ^ 1], nbias, tid);
     }
+    nraw = nraw2;
   }
   const HalfPair lp = half_pair(lsum);
   const float ltot = lp.x + lp.y;
@@ -413,9 +448,10 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
 // Backward, dQ: wavefront = 32 queries; loops over key blocks.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(1024))) char tiles[2][2 * TILE];  // per stage: K, V
-  __shared__ __attribute__((aligned(16))) float kbias[2][KT];
-  __shared__ int kfull[2][2];  // per stage and 32-key half: no key masked
+  __shared__ __attribute__((aligned(1024))) LdsKV lds;  // as in the forward
+  auto& tiles = lds.tiles;
+  auto& kbias = lds.kbias;
+  auto& kfull = lds.kfull;
 
   int qb, bh;
   attn_block((a.S + 127) / 128, qb, bh);
@@ -434,59 +470,71 @@ __global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
   const int nkb = (kend + KT - 1) / KT;
   const int q = q0 + rr;
   const __amdgpu_buffer_rsrc_t rsK = rows_rsrc(Kg, S, ld), rsV = rows_rsrc(Vg, S, ld);
-  auto bias_of = [&](int kb) {
-    const int k = kb * KT + tid;
-    return (k < kend && mrow[k] != 0) ? 0.0f : -INFINITY;
+  // Mask byte of key kb KT + tid (clamped to a valid key, so that the load
+  // is unconditional) and the key bias it gives (0 or -inf).  Wavefront 0
+  // loads the bytes of block kb + 2 during block kb and turns them into the
+  // bias of block kb + 2 at the end of block kb + 1, after the wait at that
+  // block's start: using them in the block that loads them made it wait a
+  // memory latency per block, and the other wavefronts then waited for it at
+  // the next barrier.
+  auto mask_raw = [&](int kb) { return (int)mrow[min(kb * KT + tid, S - 1)]; };
+  auto bias_from = [&](int kb, int raw) {
+    return (kb * KT + tid < kend && raw != 0) ? 0.0f : -INFINITY;
   };
+  auto bias_of = [&](int kb) { return bias_from(kb, mask_raw(kb)); };
 
+  // Set-up loads in the order that lets their latencies overlap: the
+  // wavefront's own fragments and log-sum-exp, the first streamed block,
+  // and only then the key-mask bytes, whose values the LDS set-up waits for.
+  // D = rowsum(dO * O) with O = the stored context plus its rounding
+  // residual: the rows of dS = P (dP - D) then sum to zero up to fp32 and
+  // residual rounding, as the key-bias gradient (exactly zero) requires.
+  const bf16_t* __restrict__ Olg = a.o_lo ? a.o_lo + (int64_t)b * S * h + j * HD : nullptr;
+  bf16x8_t qf[4], dof[4], of[4], olf[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    const int c = 16 * ks + 8 * hf;
+    if (q < S) {
+      qf[ks] = ld_frag(Qg + (int64_t)q * ld + c);
+      dof[ks] = ld_frag(dOg + (int64_t)q * h + c);
+      of[ks] = ld_frag(Og + (int64_t)q * h + c);
+      olf[ks] = Olg ? ld_frag(Olg + (int64_t)q * h + c) : __builtin_bit_cast(bf16x8_t, zero4());
+    } else {
+      qf[ks] = dof[ks] = of[ks] = olf[ks] = __builtin_bit_cast(bf16x8_t, zero4());
+    }
+  }
+  const float lse_q = q < S ? a.lse[(int64_t)bh * S + q] : 0.0f;
   if (nkb > 0) {
+    dma_rows(rsK, 0, ld, tiles[0], wave, lane);
+    dma_rows(rsV, 0, ld, tiles[0] + TILE, wave, lane);
     if (tid < KT) {  // wavefront 0
       const float kb0 = bias_of(0);
       kbias[0][tid] = kb0;
       store_kfull(kfull[0], kb0, tid);
     }
-    dma_rows(rsK, 0, ld, tiles[0], wave, lane);
-    dma_rows(rsV, 0, ld, tiles[0] + TILE, wave, lane);
   }
-  // D = rowsum(dO * O) with O = the stored context plus its rounding
-  // residual: the rows of dS = P (dP - D) then sum to zero up to fp32 and
-  // residual rounding, as the key-bias gradient (exactly zero) requires.
-  const bf16_t* __restrict__ Olg = a.o_lo ? a.o_lo + (int64_t)b * S * h + j * HD : nullptr;
-  bf16x8_t qf[4], dof[4];
+  int nraw = (tid < KT && nkb > 1) ? mask_raw(1) : 0;  // bytes of the next block
   float dsum = 0.0f;
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-    const int c = 16 * ks + 8 * hf;
-    bf16x8_t of, olf;
-    if (q < S) {
-      qf[ks] = ld_frag(Qg + (int64_t)q * ld + c);
-      dof[ks] = ld_frag(dOg + (int64_t)q * h + c);
-      of = ld_frag(Og + (int64_t)q * h + c);
-      olf = Olg ? ld_frag(Olg + (int64_t)q * h + c) : __builtin_bit_cast(bf16x8_t, zero4());
-    } else {
-      qf[ks] = dof[ks] = of = olf = __builtin_bit_cast(bf16x8_t, zero4());
-    }
+  for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-    for (int i = 0; i < 8; ++i) dsum += (float)dof[ks][i] * ((float)of[i] + (float)olf[i]);
-  }
+    for (int i = 0; i < 8; ++i) dsum += (float)dof[ks][i] * ((float)of[ks][i] + (float)olf[ks][i]);
   {
     const HalfPair dp2 = half_pair(dsum);
     dsum = dp2.x + dp2.y;  // D = rowsum(dO * O) of query q
   }
   if (hf == 0 && q < S) a.dsum[(int64_t)bh * S + q] = dsum;
-  const float lse_q = q < S ? a.lse[(int64_t)bh * S + q] : 0.0f;
 
   f32x16_t dq[2] = {zero16(), zero16()};  // dQ^T: dims x queries
   for (int kb = 0; kb < nkb; ++kb) {
     const int st = kb & 1;
     wait_all();
     __syncthreads();
-    float nbias = 0.0f;
     if (kb + 1 < nkb) {
-      if (tid < KT) nbias = bias_of(kb + 1);
       dma_rows(rsK, (kb + 1) * KT, ld, tiles[st ^ 1], wave, lane);
       dma_rows(rsV, (kb + 1) * KT, ld, tiles[st ^ 1] + TILE, wave, lane);
     }
+    const int nraw2 = (tid < KT && kb + 2 < nkb) ? mask_raw(kb + 2) : 0;
     const char* Ks = tiles[st];
     const char* Vs = tiles[st] + TILE;
 #pragma unroll
@@ -525,9 +573,11 @@ __global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
       }
     }
     if (kb + 1 < nkb && tid < KT) {
+      const float nbias = bias_from(kb + 1, nraw);
       kbias[st ^ 1][tid] = nbias;
       store_kfull(kfull[st ^ 1], nbias, tid);
     }
+    nraw = nraw2;
   }
   __syncthreads();  // the ring becomes the output staging area
   bf16_t* stage = (bf16_t*)&tiles[0][0] + wave * 32 * LD;
@@ -544,8 +594,14 @@ __global__ __launch_bounds__(256, 3) void attn_bwd_dq_kernel(AttnArgs a) {
 constexpr int QB = 2 * KT;
 constexpr int QTILE = QB * HD * 2;
 __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(1024))) char tiles[2][2 * QTILE];  // per stage: Q, dO
-  __shared__ __attribute__((aligned(16))) float rowv[2][2][QB];        // per stage: lse, D
+  // One LDS object (see LdsKV): Q, dO per stage; lse and D per stage.
+  struct LdsQD {
+    char tiles[2][2 * QTILE];
+    float rowv[2][2][QB];
+  };
+  __shared__ __attribute__((aligned(1024))) LdsQD lds;
+  auto& tiles = lds.tiles;
+  auto& rowv = lds.rowv;
 
   int kb128, bh;
   attn_block((a.S + 127) / 128, kb128, bh);
@@ -560,27 +616,29 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
   const bf16_t* __restrict__ dOg = a.dout + (int64_t)b * S * h + j * HD;
   const int kend = a.kext[b];
   const int key = k0 + rr;
-  const bool kvalid = key < kend && a.mask[(int64_t)b * S + key] != 0;
   const bool block_live = kb128 * 128 < kend;  // uniform over the block
   const int nqb = block_live ? (S + QB - 1) / QB : 0;
   const __amdgpu_buffer_rsrc_t rsQ = rows_rsrc(Qg, S, ld), rsD = rows_rsrc(dOg, S, h);
   // threads 0-127 carry lse, 128-255 -D of query block qb (rows past S:
   // P = 0)
   static_assert(2 * QB == 256, "one value per thread");
-  auto rowval = [&](int qb) {
-    const int qq = qb * QB + (tid & (QB - 1));
-    if (tid < QB) return qq < S ? a.lse[(int64_t)bh * S + qq] : INFINITY;
-    return qq < S ? -a.dsum[(int64_t)bh * S + qq] : -0.0f;
+  // The load (row clamped to a valid query, so that it is unconditional)
+  // and the value it gives, kept apart as for the key mask of the forward:
+  // the values of block qb + 2 are loaded during block qb and stored at the
+  // end of block qb + 1.
+  auto row_raw = [&](int qb) {
+    const int qq = min(qb * QB + (tid & (QB - 1)), S - 1);
+    return (tid < QB ? a.lse : a.dsum)[(int64_t)bh * S + qq];
   };
-  // Initial score accumulator: 0, or -inf for a masked key (the lane's
-  // column), which makes its probabilities exp2(-inf) = 0.
-  const f32x16_t s0 = splat16(kvalid ? 0.0f : -INFINITY);
-
-  if (nqb > 0) {
-    rowv[0][tid / QB][tid & (QB - 1)] = rowval(0);
-    dma_rows<QB>(rsQ, 0, ld, tiles[0], wave, lane);
-    dma_rows<QB>(rsD, 0, h, tiles[0] + QTILE, wave, lane);
-  }
+  auto row_from = [&](int qb, float raw) {
+    const bool in = qb * QB + (tid & (QB - 1)) < S;
+    if (tid < QB) return in ? raw : INFINITY;
+    return in ? -raw : -0.0f;
+  };
+  auto rowval = [&](int qb) { return row_from(qb, row_raw(qb)); };
+  // Set-up loads in the order that lets their latencies overlap: the
+  // wavefront's own fragments, the first streamed block, and only then the
+  // per-query values, whose LDS store waits for them.
   bf16x8_t kf[4], vf[4];
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
@@ -592,18 +650,28 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
       kf[ks] = vf[ks] = __builtin_bit_cast(bf16x8_t, zero4());
     }
   }
+  const int kraw = a.mask[(int64_t)b * S + min(key, S - 1)];
+  if (nqb > 0) {
+    dma_rows<QB>(rsQ, 0, ld, tiles[0], wave, lane);
+    dma_rows<QB>(rsD, 0, h, tiles[0] + QTILE, wave, lane);
+    rowv[0][tid / QB][tid & (QB - 1)] = rowval(0);
+  }
+  float nraw = nqb > 1 ? row_raw(1) : 0.0f;  // values of the next block
+  // Initial score accumulator: 0, or -inf for a masked key (the lane's
+  // column), which makes its probabilities exp2(-inf) = 0.
+  const bool kvalid = key < kend && kraw != 0;
+  const f32x16_t s0 = splat16(kvalid ? 0.0f : -INFINITY);
   f32x16_t dv[2] = {zero16(), zero16()}, dk[2] = {zero16(), zero16()};  // dims x keys
 
   for (int qb = 0; qb < nqb; ++qb) {
     const int st = qb & 1;
     wait_all();
     __syncthreads();
-    float nrow = 0.0f;
     if (qb + 1 < nqb) {
-      nrow = rowval(qb + 1);
       dma_rows<QB>(rsQ, (qb + 1) * QB, ld, tiles[st ^ 1], wave, lane);
       dma_rows<QB>(rsD, (qb + 1) * QB, h, tiles[st ^ 1] + QTILE, wave, lane);
     }
+    const float nraw2 = qb + 2 < nqb ? row_raw(qb + 2) : 0.0f;
     const char* Qs = tiles[st];
     const char* dOs = tiles[st] + QTILE;
 #pragma unroll
@@ -646,7 +714,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
         }
       }
     }
-    if (qb + 1 < nqb) rowv[st ^ 1][tid / QB][tid & (QB - 1)] = nrow;
+    if (qb + 1 < nqb) rowv[st ^ 1][tid / QB][tid & (QB - 1)] = row_from(qb + 1, nraw);
+    nraw = nraw2;
   }
   __syncthreads();  // the ring becomes the output staging area
   bf16_t* stage = (bf16_t*)&tiles[0][0] + wave * 32 * LD;
