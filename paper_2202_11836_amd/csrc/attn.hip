@@ -185,7 +185,9 @@ __device__ __forceinline__ void store_rows_t(const f32x16_t acc[2], float mul, b
       const uint32_t hi = pack_bf16x2(v[2], v[3]);
       *(u32x2_t*)(stage + rr * LD + col) = u32x2_t{lo, hi};
     }
-  __builtin_amdgcn_s_waitcnt(0);
+  // The staged values must be in LDS before other lanes read them; global
+  // stores still in flight (a previous call's) need not be waited for.
+  lds_wait();
   __builtin_amdgcn_wave_barrier();
   // lane owns column chunk (lane & 7) * 8 and rows (lane >> 3) + 8 i
   float cs[8] = {0, 0, 0, 0, 0, 0, 0, 0};
@@ -438,7 +440,7 @@ __global__ __launch_bounds__(256, 4) void attn_fwd_kernel(AttnArgs a) {
   bf16_t* stage = (bf16_t*)&tiles[0][0] + wave * 32 * LD;
   store_rows_t(acc, inv, stage, a.out + (int64_t)b * S * h + j * HD, h, q0, S, nullptr);
   if (a.out_lo) {
-    __builtin_amdgcn_s_waitcnt(0);
+    lds_wait();
     __builtin_amdgcn_wave_barrier();
     store_rows_t(acc, inv, stage, a.out_lo + (int64_t)b * S * h + j * HD, h, q0, S, nullptr, true);
   }
